@@ -1,0 +1,140 @@
+/*
+ * sinkhorn.h -- C ABI of the MI355X (gfx950) batched log-domain Sinkhorn library.
+ *
+ * Method: Viehmann, "Implementation of batched Sinkhorn iterations for
+ * entropy-regularized Wasserstein loss" (arXiv:1907.01729).  For a batch of
+ * histogram pairs (mu_b, nu_b) and a cost C (shared, or one per sample) the
+ * library runs the log-domain Sinkhorn iteration (Section 3, eq. (log_sk), with
+ * the sign of the batched form in Section 4), returns the log-scalings, the
+ * loss E^0 (Section 5) and the marginal error, and computes the
+ * Lagrange-multiplier gradient (Section 2).
+ *
+ * Conventions shared by every entry point
+ *   - Every array argument is a DEVICE pointer to contiguous row-major data
+ *     (fp32 unless stated).  The caller owns every buffer; the library never
+ *     allocates, frees or synchronises, and keeps no state between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Work is enqueued asynchronously; results are valid once the stream has
+ *     been synchronised.  Calls that overlap on one workspace race.
+ *   - Errors are detected on the host before anything is launched (launch
+ *     failures map to SK_ERR_HIP).  On error, output contents are unspecified.
+ *     No C++ exception or abort crosses this interface.
+ *   - Preconditions NOT checked (they would need a device synchronisation):
+ *     mu, nu >= 0 with sum mu = sum nu = 1 (Section 1: probability measures),
+ *     finite C.  Zero masses are allowed: their log-scalings are -inf
+ *     (Section 3) and their gradients 0.  Non-finite inputs propagate.
+ *
+ * Notation.  alpha = log u, beta = log v (natural log, dimensionless), so the
+ * plan is P_ij = exp(alpha_i + beta_j - C_ij / lambda)   (Section 1,
+ * eq. (pij_form) with P = diag(u) K diag(v), K = exp(-C/lambda)).
+ * The dual potentials in cost units are lambda*alpha and lambda*beta.
+ */
+#ifndef SINKHORN_H_
+#define SINKHORN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__) || defined(__clang__)
+#define SK_API __attribute__((visibility("default")))
+#else
+#define SK_API
+#endif
+
+typedef enum {
+    SK_OK = 0,
+    SK_ERR_NULLPTR = -1,   /* a required pointer is NULL                     */
+    SK_ERR_SHAPE = -2,     /* B < 0, d1 < 1, d2 < 1, or sizes overflow        */
+    SK_ERR_LAMBDA = -3,    /* lambda not finite and > 0                       */
+    SK_ERR_ITERS = -4,     /* n_iter < 0, or tol not finite                   */
+    SK_ERR_WORKSPACE = -5, /* ws_bytes < sinkhorn_workspace_bytes(p)          */
+    SK_ERR_HIP = -6        /* a HIP launch failed (e.g. device is not gfx950) */
+} sk_status;
+
+typedef struct {
+    int32_t B;          /* batch size, >= 0 (0: nothing to do)                      */
+    int32_t d1, d2;     /* support sizes of mu and nu, >= 1                         */
+    int32_t c_batched;  /* 0: C is [d1, d2], shared by the batch (Section 4);
+                           1: C is [B, d1, d2], one cost per sample               */
+    float lambda;       /* entropic regularisation, > 0, in cost units (Section 1) */
+    int32_t n_iter;     /* number of full iterations (v-update, then u-update)      */
+    float tol;          /* <= 0: always run n_iter (the paper's choice, Section 5);
+                           > 0: per sample, stop after the first iteration
+                           k < n_iter whose iterate has marginal L1 error <= tol   */
+} sk_problem;
+
+/*
+ * Bytes of device workspace sinkhorn_forward needs for problem *p (0 when the
+ * problem runs entirely on-chip).  Returns 0 for an invalid problem.
+ */
+SK_API size_t sinkhorn_workspace_bytes(const sk_problem *p);
+
+/*
+ * Forward: log-domain Sinkhorn (Section 3 and 4) followed by the loss
+ * (Section 5).  Iteration k (1-based) performs
+ *     beta_j  <- log nu_j - LSE_i(alpha_i - C_ij/lambda)     (v-update)
+ *     alpha_i <- log mu_i - LSE_j(beta_j  - C_ij/lambda)     (u-update)
+ * from alpha^0 = 0 on the support of mu (-inf off it).  With n_iter = 0,
+ * alpha = beta = 0 on the supports.
+ *
+ *   mu        [B, d1]              input histograms
+ *   nu        [B, d2]
+ *   C         [d1, d2] or [B, d1, d2] (see c_batched)
+ *   alpha     [B, d1]   out        log u of the returned iterate
+ *   beta      [B, d2]   out        log v of the returned iterate
+ *   loss      [B]       out        E^0 = sum_ij P_ij C_ij (Section 5)
+ *   marg_err  [B]       out        ||P 1 - mu||_1 + ||P^T 1 - nu||_1
+ *   iters     [B] int32 out        iterations run per sample (n_iter unless
+ *                                  the early stop fired)
+ *   workspace, ws_bytes            device scratch of at least
+ *                                  sinkhorn_workspace_bytes(p) bytes (may be
+ *                                  NULL when that is 0); contents on entry are
+ *                                  irrelevant, on exit unspecified
+ */
+SK_API sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu,
+                           const float *C, float *alpha, float *beta, float *loss,
+                           float *marg_err, int32_t *iters, void *workspace,
+                           size_t ws_bytes, void *stream);
+
+/*
+ * Backward (Section 2): the Lagrange-multiplier gradient of the entropic
+ * objective W_lambda(mu, nu) = min_U E^lambda, taken at the iterate the
+ * forward returned (Section 5 explains why this is used for the E^0 loss).
+ * With g = grad_loss[b]:
+ *   grad_mu[b,i] = g * lambda * (alpha[b,i] - mean over the support of mu_b of
+ *                  alpha[b,.]),  0 where mu[b,i] == 0;
+ *   grad_nu      likewise with beta and nu;
+ *   grad_C (optional, may be NULL): d W_lambda / d C = P, i.e.
+ *                  g * P_b           for c_batched (shape [B, d1, d2]),
+ *                  sum_b g_b * P_b   for a shared C (shape [d1, d2]).
+ * alpha and beta are the forward's outputs; n_iter and tol are ignored.
+ * Needs no workspace.  Deterministic (fixed reduction order, no atomics).
+ */
+SK_API sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss,
+                            const float *mu, const float *nu, const float *C,
+                            const float *alpha, const float *beta,
+                            float *grad_mu, float *grad_nu, float *grad_C,
+                            void *stream);
+
+/* Static description of a status code (never NULL). */
+SK_API const char *sinkhorn_status_string(sk_status s);
+
+/*
+ * Which kernel family sinkhorn_forward uses for *p:
+ *   1 = resident (one wavefront per problem; C and potentials on-chip for the
+ *       whole iteration; max(d1, d2) <= 128),
+ *   2 = tiled sweep (one pass over C per iteration, column partials merged
+ *       across row blocks).
+ * Returns 0 for an invalid problem.
+ */
+SK_API int32_t sinkhorn_regime(const sk_problem *p);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SINKHORN_H_ */

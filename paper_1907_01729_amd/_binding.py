@@ -1,0 +1,177 @@
+"""ctypes binding of include/sinkhorn.h (argument marshalling only)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libsinkhorn_hip.so")
+_lib = None
+
+SK_STATUS = {
+    0: "SK_OK",
+    -1: "SK_ERR_NULLPTR",
+    -2: "SK_ERR_SHAPE",
+    -3: "SK_ERR_LAMBDA",
+    -4: "SK_ERR_ITERS",
+    -5: "SK_ERR_WORKSPACE",
+    -6: "SK_ERR_HIP",
+}
+
+EXPORTED = (
+    "sinkhorn_workspace_bytes",
+    "sinkhorn_forward",
+    "sinkhorn_backward",
+    "sinkhorn_status_string",
+    "sinkhorn_regime",
+)
+
+
+class SinkhornError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {SK_STATUS.get(status, status)} ({sinkhorn_status_string(status)})")
+
+
+class SkProblem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32),
+        ("d1", ctypes.c_int32),
+        ("d2", ctypes.c_int32),
+        ("c_batched", ctypes.c_int32),
+        ("lam", ctypes.c_float),
+        ("n_iter", ctypes.c_int32),
+        ("tol", ctypes.c_float),
+    ]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libsinkhorn_hip.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            f"{_LIB_PATH} is missing: build it with `python paper_1907_01729_amd/build.py` "
+            "(or __graft_entry__.build()); there is no CPU fallback")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    PP = ctypes.POINTER(SkProblem)
+    lib.sinkhorn_workspace_bytes.argtypes = [PP]
+    lib.sinkhorn_workspace_bytes.restype = ctypes.c_size_t
+    lib.sinkhorn_forward.argtypes = [PP, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.sinkhorn_forward.restype = ctypes.c_int
+    lib.sinkhorn_backward.argtypes = [PP, P, P, P, P, P, P, P, P, P, P]
+    lib.sinkhorn_backward.restype = ctypes.c_int
+    lib.sinkhorn_status_string.argtypes = [ctypes.c_int]
+    lib.sinkhorn_status_string.restype = ctypes.c_char_p
+    lib.sinkhorn_regime.argtypes = [PP]
+    lib.sinkhorn_regime.restype = ctypes.c_int32
+    _lib = lib
+    return lib
+
+
+def problem(B, d1, d2, c_batched, lam, n_iter, tol=0.0) -> SkProblem:
+    return SkProblem(int(B), int(d1), int(d2), int(c_batched), float(lam), int(n_iter), float(tol))
+
+
+def sinkhorn_status_string(status: int) -> str:
+    return load_library().sinkhorn_status_string(int(status)).decode()
+
+
+def sinkhorn_workspace_bytes(B, d1, d2, c_batched, lam, n_iter, tol=0.0) -> int:
+    p = problem(B, d1, d2, c_batched, lam, n_iter, tol)
+    return int(load_library().sinkhorn_workspace_bytes(ctypes.byref(p)))
+
+
+def sinkhorn_regime(B, d1, d2, c_batched, lam=1.0, n_iter=1, tol=0.0) -> int:
+    p = problem(B, d1, d2, c_batched, lam, n_iter, tol)
+    return int(load_library().sinkhorn_regime(ctypes.byref(p)))
+
+
+def _dev(t: torch.Tensor, name: str, dtype=torch.float32) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _shapes(mu, nu, C):
+    if mu.dim() != 2 or nu.dim() != 2 or mu.shape[0] != nu.shape[0]:
+        raise ValueError(f"mu must be [B,d1] and nu [B,d2], got {tuple(mu.shape)} {tuple(nu.shape)}")
+    B, d1 = mu.shape
+    d2 = nu.shape[1]
+    if C.dim() == 2:
+        C = C.unsqueeze(0)
+    if C.dim() != 3 or tuple(C.shape[1:]) != (d1, d2) or C.shape[0] not in (1, B):
+        raise ValueError(f"C must be [d1,d2], [1,d1,d2] or [B,d1,d2], got {tuple(C.shape)}")
+    c_batched = int(C.shape[0] == B and B != 1)
+    return B, d1, d2, c_batched
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(device, stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def sinkhorn_forward(mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None):
+    """Run the forward on the GPU.
+
+    mu [B,d1], nu [B,d2], C [d1,d2] | [1,d1,d2] | [B,d1,d2]: float32 CUDA tensors.
+    Returns dict(alpha [B,d1], beta [B,d2], loss [B], marg_err [B], iters [B] int32).
+    """
+    lib = load_library()
+    _dev(mu, "mu"), _dev(nu, "nu"), _dev(C, "C")
+    B, d1, d2, cb = _shapes(mu, nu, C)
+    p = problem(B, d1, d2, cb, lam, n_iter, tol)
+    dev = mu.device
+    f = dict(device=dev, dtype=torch.float32)
+    alpha = torch.empty((B, d1), **f)
+    beta = torch.empty((B, d2), **f)
+    loss = torch.empty((B,), **f)
+    merr = torch.empty((B,), **f)
+    iters = torch.empty((B,), device=dev, dtype=torch.int32)
+    need = int(lib.sinkhorn_workspace_bytes(ctypes.byref(p)))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
+    st = lib.sinkhorn_forward(ctypes.byref(p), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha), _ptr(beta), _ptr(loss),
+                              _ptr(merr), _ptr(iters), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+                              _stream(dev, stream))
+    if st != 0:
+        raise SinkhornError(st, "sinkhorn_forward")
+    return dict(alpha=alpha, beta=beta, loss=loss, marg_err=merr, iters=iters)
+
+
+def sinkhorn_backward(grad_loss, mu, nu, C, lam, alpha, beta, grad_C=False, stream=None):
+    """Multiplier gradient (Section 2) on the GPU: dict(grad_mu, grad_nu[, grad_C])."""
+    lib = load_library()
+    for t, n in ((grad_loss, "grad_loss"), (mu, "mu"), (nu, "nu"), (C, "C"), (alpha, "alpha"), (beta, "beta")):
+        _dev(t, n)
+    B, d1, d2, cb = _shapes(mu, nu, C)
+    p = problem(B, d1, d2, cb, lam, 0, 0.0)
+    dev = mu.device
+    f = dict(device=dev, dtype=torch.float32)
+    gmu = torch.empty((B, d1), **f)
+    gnu = torch.empty((B, d2), **f)
+    gC = torch.empty(((B if cb else 1), d1, d2), **f) if grad_C else None
+    st = lib.sinkhorn_backward(ctypes.byref(p), _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
+                               _ptr(beta), _ptr(gmu), _ptr(gnu), _ptr(gC), _stream(dev, stream))
+    if st != 0:
+        raise SinkhornError(st, "sinkhorn_backward")
+    out = dict(grad_mu=gmu, grad_nu=gnu)
+    if grad_C:
+        out["grad_C"] = gC
+    return out

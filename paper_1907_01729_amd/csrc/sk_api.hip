@@ -1,0 +1,114 @@
+// sk_api.hip -- the C ABI declared in include/sinkhorn.h: argument checks,
+// regime dispatch and launches.  No allocation, no synchronisation.
+#include <math.h>
+#include <stdint.h>
+
+#include "sk_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxDim = 1 << 24;
+
+sk_status check_problem(const sk_problem *p) {
+    if (!p) return SK_ERR_NULLPTR;
+    if (p->B < 0 || p->d1 < 1 || p->d2 < 1 || p->d1 > kMaxDim || p->d2 > kMaxDim) return SK_ERR_SHAPE;
+    if (p->c_batched != 0 && p->c_batched != 1) return SK_ERR_SHAPE;
+    const int64_t cells = (int64_t)p->d1 * p->d2;
+    if (cells > (int64_t(1) << 40) || (int64_t)p->B * cells > (int64_t(1) << 46)) return SK_ERR_SHAPE;
+    if (!(p->lambda > 0.f) || !isfinite(p->lambda)) return SK_ERR_LAMBDA;
+    if (p->n_iter < 0 || !isfinite(p->tol)) return SK_ERR_ITERS;
+    return SK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sinkhorn_status_string(sk_status s) {
+    switch (s) {
+        case SK_OK: return "ok";
+        case SK_ERR_NULLPTR: return "a required pointer is NULL";
+        case SK_ERR_SHAPE: return "invalid shape (B < 0, d1 < 1, d2 < 1, c_batched not 0/1, or size overflow)";
+        case SK_ERR_LAMBDA: return "lambda must be finite and > 0";
+        case SK_ERR_ITERS: return "n_iter must be >= 0 and tol finite";
+        case SK_ERR_WORKSPACE: return "workspace smaller than sinkhorn_workspace_bytes()";
+        case SK_ERR_HIP: return "HIP launch failed (is the device a gfx950?)";
+    }
+    return "unknown status";
+}
+
+int32_t sinkhorn_regime(const sk_problem *p) {
+    if (check_problem(p) != SK_OK) return 0;
+    return sk::resident_fits(p->d1, p->d2) ? 1 : 2;
+}
+
+size_t sinkhorn_workspace_bytes(const sk_problem *p) {
+    if (check_problem(p) != SK_OK) return 0;
+    if (sk::resident_fits(p->d1, p->d2)) return 0;
+    return sk::tiled_workspace_bytes(p->B, p->d1, p->d2, p->c_batched);
+}
+
+sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu, const float *C, float *alpha,
+                           float *beta, float *loss, float *marg_err, int32_t *iters, void *workspace,
+                           size_t ws_bytes, void *stream) {
+    sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (p->B == 0) return SK_OK;
+    if (!mu || !nu || !C || !alpha || !beta || !loss || !marg_err || !iters) return SK_ERR_NULLPTR;
+    const size_t need = sinkhorn_workspace_bytes(p);
+    if (ws_bytes < need) return SK_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return SK_ERR_NULLPTR;
+
+    sk::FwdArgs a;
+    a.mu = mu;
+    a.nu = nu;
+    a.C = C;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.loss = loss;
+    a.marg_err = marg_err;
+    a.iters = iters;
+    a.B = p->B;
+    a.d1 = p->d1;
+    a.d2 = p->d2;
+    a.n_iter = p->n_iter;
+    a.c_batched = p->c_batched;
+    a.lambda = p->lambda;
+    a.tol = p->tol;
+    a.s = sk::kLog2eHost / p->lambda;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = sk::resident_fits(p->d1, p->d2) ? sk::launch_resident(a, s) : sk::launch_tiled(a, workspace, s);
+    return e == hipSuccess ? SK_OK : SK_ERR_HIP;
+}
+
+sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu,
+                            const float *C, const float *alpha, const float *beta, float *grad_mu, float *grad_nu,
+                            float *grad_C, void *stream) {
+    sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (p->B == 0) return SK_OK;
+    if (!grad_loss || !mu || !nu || !alpha || !beta || !grad_mu || !grad_nu) return SK_ERR_NULLPTR;
+    if (grad_C && !C) return SK_ERR_NULLPTR;
+
+    sk::BwdArgs a;
+    a.grad_loss = grad_loss;
+    a.mu = mu;
+    a.nu = nu;
+    a.C = C;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.grad_mu = grad_mu;
+    a.grad_nu = grad_nu;
+    a.grad_C = grad_C;
+    a.B = p->B;
+    a.d1 = p->d1;
+    a.d2 = p->d2;
+    a.c_batched = p->c_batched;
+    a.lambda = p->lambda;
+    a.s = sk::kLog2eHost / p->lambda;
+    hipError_t e = sk::launch_backward(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SK_OK : SK_ERR_HIP;
+}
+
+}  // extern "C"

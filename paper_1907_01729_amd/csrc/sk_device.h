@@ -1,0 +1,71 @@
+// sk_device.h -- device helpers shared by the gfx950 Sinkhorn kernels.
+//
+// Base-2 arithmetic throughout: potentials are kept as a = alpha*log2(e),
+// b = beta*log2(e) and the cost as cl = -C*log2(e)/lambda, so every plan
+// entry P_ij = exp(alpha_i + beta_j - C_ij/lambda) is a single v_exp_f32 of
+// (a_i + b_j + cl_ij).  Logarithms of sums use v_log_f32 (base 2).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sk {
+
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr float kLn2 = 0.69314718055994530942f;
+// A sum of exponentials shifted by the previous potentials is trusted when it
+// lies in [2^-64, 2^64]: each term it may have lost to underflow (< 2^-126) is
+// then below 2^-62 of the sum.  Outside that range the exact
+// max-then-sum logsumexp is used instead.
+constexpr float kSumLo = 5.42101086242752217e-20f;  // 2^-64
+constexpr float kSumHi = 1.84467440737095516e19f;   // 2^64
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
+
+// v_exp_f32 / v_log_f32: base-2 hardware transcendentals.
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float lg2(float x) { return __builtin_amdgcn_logf(x); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// DPP controls used below.
+constexpr int kQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]   : lane ^ 1
+constexpr int kQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]   : lane ^ 2
+constexpr int kHalfMirror = 0x141;   // row_half_mirror       : lane -> 7 - lane (within 8)
+constexpr int kRowRor8 = 0x128;      // row_ror:8             : lane ^ 8 (within 16)
+
+// All-reduce over the 8 consecutive lanes 8p..8p+7.  Every butterfly step adds
+// two values in both orders' IEEE-equal way, so all 8 lanes end bit-identical.
+__device__ __forceinline__ float sum_q(float v) {
+    v += dpp<kQuadXor1>(v);
+    v += dpp<kQuadXor2>(v);
+    v += dpp<kHalfMirror>(v);
+    return v;
+}
+__device__ __forceinline__ float max_q(float v) {
+    v = fmaxf(v, dpp<kQuadXor1>(v));
+    v = fmaxf(v, dpp<kQuadXor2>(v));
+    v = fmaxf(v, dpp<kHalfMirror>(v));
+    return v;
+}
+// All-reduce over the 8 lanes q, q+8, ..., q+56 (same lane & 7).
+__device__ __forceinline__ float sum_p(float v) {
+    v += dpp<kRowRor8>(v);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    return v;
+}
+__device__ __forceinline__ float max_p(float v) {
+    v = fmaxf(v, dpp<kRowRor8>(v));
+    v = fmaxf(v, __shfl_xor(v, 16));
+    v = fmaxf(v, __shfl_xor(v, 32));
+    return v;
+}
+// Whole-wavefront all-reduce (bit-identical on every lane).
+__device__ __forceinline__ float wave_sum(float v) { return sum_p(sum_q(v)); }
+__device__ __forceinline__ float wave_max(float v) { return max_p(max_q(v)); }
+
+}  // namespace sk

@@ -1,0 +1,42 @@
+// sk_internal.h -- host-side launchers shared between the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/sinkhorn.h"
+
+namespace sk {
+
+constexpr float kLog2eHost = 1.44269504088896340736f;
+
+struct FwdArgs {
+    const float *mu, *nu, *C;
+    float *alpha, *beta, *loss, *marg_err;
+    int32_t *iters;
+    int B, d1, d2, n_iter, c_batched;
+    float lambda, tol;
+    float s;  // log2(e) / lambda
+};
+
+struct BwdArgs {
+    const float *grad_loss, *mu, *nu, *C, *alpha, *beta;
+    float *grad_mu, *grad_nu, *grad_C;
+    int B, d1, d2, c_batched;
+    float lambda;
+    float s;  // log2(e) / lambda
+};
+
+// Largest support size the resident (one wavefront per problem) kernel takes.
+constexpr int kResidentMaxD = 128;
+
+bool resident_fits(int d1, int d2);
+hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
+
+size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched);
+hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);
+
+hipError_t launch_backward(const BwdArgs &a, hipStream_t st);
+
+}  // namespace sk

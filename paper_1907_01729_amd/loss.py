@@ -1,0 +1,41 @@
+"""autograd wrapper: the loss E^0 with the Lagrange-multiplier gradient.
+
+Section 5 of the paper: the forward returns E^0(P) = sum P C at the
+approximate minimiser of E^lambda, the backward returns the gradient of
+E^lambda obtained from the multipliers (Section 2), not the gradient of E^0.
+"""
+from __future__ import annotations
+
+import torch
+
+from ._binding import sinkhorn_backward, sinkhorn_forward
+
+
+class SinkhornLoss(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, mu, nu, C, lam, n_iter, tol):
+        out = sinkhorn_forward(mu.contiguous(), nu.contiguous(), C.contiguous(), lam, n_iter, tol)
+        ctx.save_for_backward(mu, nu, C, out["alpha"], out["beta"])
+        ctx.lam = lam
+        ctx.mark_non_differentiable(out["alpha"], out["beta"], out["marg_err"], out["iters"])
+        return out["loss"], out["alpha"], out["beta"], out["marg_err"], out["iters"]
+
+    @staticmethod
+    def backward(ctx, grad_loss, *unused):
+        mu, nu, C, alpha, beta = ctx.saved_tensors
+        want_C = ctx.needs_input_grad[2]
+        g = sinkhorn_backward(grad_loss.contiguous(), mu.contiguous(), nu.contiguous(), C.contiguous(), ctx.lam,
+                              alpha, beta, grad_C=want_C)
+        gC = None
+        if want_C:
+            gC = g["grad_C"].reshape(C.shape) if C.dim() == 3 or g["grad_C"].shape[0] == 1 else g["grad_C"]
+            gC = gC.reshape(C.shape)
+        return g["grad_mu"], g["grad_nu"], gC, None, None, None
+
+
+def sinkhorn_loss(mu, nu, C, lam, n_iter, tol=0.0, return_state=False):
+    """Per-sample loss E^0 [B]; differentiable w.r.t. mu, nu and C."""
+    loss, alpha, beta, merr, iters = SinkhornLoss.apply(mu, nu, C, lam, n_iter, tol)
+    if return_state:
+        return loss, dict(alpha=alpha, beta=beta, marg_err=merr, iters=iters)
+    return loss

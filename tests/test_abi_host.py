@@ -1,0 +1,103 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/sinkhorn.h declares, and rejects invalid arguments on
+the host before anything is launched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_1907_01729_amd as sk
+from paper_1907_01729_amd import _binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sinkhorn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SK_API\s+[\w\s\*]+?\b(sinkhorn_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_abi():
+    assert declared_functions() == sorted(_binding.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = sk.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", sk.library_path()], capture_output=True, text=True,
+                         check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if l.strip()}
+    for name in declared_functions():
+        assert name in exported, name
+    # nothing else of the library's own leaks into the dynamic symbol table
+    assert not [s for s in exported if s.startswith("_ZN2sk")]
+
+
+def test_status_strings():
+    for code in range(-6, 1):
+        assert sk.sinkhorn_status_string(code)
+    assert "lambda" in sk.sinkhorn_status_string(-3)
+    assert sk.sinkhorn_status_string(-99) == "unknown status"
+
+
+def test_regime_and_workspace_queries():
+    assert sk.sinkhorn_regime(4, 10, 10, 0) == 1
+    assert sk.sinkhorn_regime(1024, 100, 100, 0) == 1
+    assert sk.sinkhorn_regime(4, 128, 128, 1) == 1
+    assert sk.sinkhorn_regime(4, 129, 10, 0) == 2
+    assert sk.sinkhorn_regime(4, 10, 10, 0, lam=0.0) == 0
+    assert sk.sinkhorn_workspace_bytes(4, 10, 10, 0, 0.1, 100) == 0
+    assert sk.sinkhorn_workspace_bytes(256, 784, 784, 0, 0.01, 300) > 0
+    assert sk.sinkhorn_workspace_bytes(-1, 784, 784, 0, 0.01, 300) == 0
+
+
+def _fwd(p, ptr=None, ws=0):
+    lib = sk.load_library()
+    v = ctypes.c_void_p(ptr) if ptr else None
+    return lib.sinkhorn_forward(ctypes.byref(p), v, v, v, v, v, v, v, v, v, ctypes.c_size_t(ws), None)
+
+
+def _bwd(p, ptr=None):
+    lib = sk.load_library()
+    v = ctypes.c_void_p(ptr) if ptr else None
+    return lib.sinkhorn_backward(ctypes.byref(p), v, v, v, v, v, v, v, v, None, None)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((4, 0, 10, 0, 0.1, 10), -2),
+    ((4, 10, 0, 0, 0.1, 10), -2),
+    ((-1, 10, 10, 0, 0.1, 10), -2),
+    ((4, 10, 10, 2, 0.1, 10), -2),
+    ((4, 10, 10, 0, 0.0, 10), -3),
+    ((4, 10, 10, 0, -1.0, 10), -3),
+    ((4, 10, 10, 0, float("inf"), 10), -3),
+    ((4, 10, 10, 0, float("nan"), 10), -3),
+    ((4, 10, 10, 0, 0.1, -1), -4),
+])
+def test_invalid_problems_rejected_on_host(args, code):
+    p = _binding.problem(*args)
+    assert _fwd(p) == code
+    if code != -4:  # backward ignores n_iter
+        assert _bwd(p) == code
+
+
+def test_invalid_tol_and_null_pointers():
+    assert _fwd(_binding.problem(4, 10, 10, 0, 0.1, 10, float("nan"))) == -4
+    assert _fwd(_binding.problem(4, 10, 10, 0, 0.1, 10)) == -1
+    assert _bwd(_binding.problem(4, 10, 10, 0, 0.1, 10)) == -1
+    lib = sk.load_library()
+    assert lib.sinkhorn_forward(None, None, None, None, None, None, None, None, None, None, 0, None) == -1
+    # B == 0 is a no-op that succeeds without touching any pointer
+    assert _fwd(_binding.problem(0, 10, 10, 0, 0.1, 10)) == 0
+
+
+def test_workspace_too_small_rejected_before_launch():
+    p = _binding.problem(8, 784, 784, 0, 0.01, 10)
+    need = sk.sinkhorn_workspace_bytes(8, 784, 784, 0, 0.01, 10)
+    assert need > 0
+    # non-NULL (never dereferenced) pointers so that only the size check fires
+    assert _fwd(p, ptr=0x1000, ws=need - 1) == -5

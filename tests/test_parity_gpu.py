@@ -1,0 +1,212 @@
+"""GPU parity: the HIP library (through the C ABI) against the fp64 oracle on
+identical seeded fp32 inputs.  Tolerances (written here, per the build target):
+loss relative error <= 1e-4, potentials absolute error <= 1e-3 after fixing the
+additive gauge, gradients relative error <= 1e-3."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1907_01729_amd as sk
+import workloads
+from parity_util import GRAD_RTOL, LOSS_RTOL, POT_ATOL, gauge_fixed_errors, loss_rel_err, rel_err_rows
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _gpu(prob, sample=None):
+    mu, nu, C = prob.mu, prob.nu, prob.C
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    out = sk.sinkhorn_forward(t(mu), t(nu), t(C), prob.lam, prob.n_iter, prob.tol)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def _subset(prob, idx):
+    C = prob.C[idx] if prob.c_batched else prob.C
+    return prob.mu[idx], prob.nu[idx], C
+
+
+def check_forward(prob, gpu=None, idx=None, pot_atol=POT_ATOL, merr_atol=2e-5, merr_rtol=5e-2):
+    """Compare a GPU forward with the oracle on samples idx (all by default),
+    at the GPU's per-sample iteration counts."""
+    _say(f"[parity] {prob.name} B={prob.B} d1={prob.d1} d2={prob.d2} lam={prob.lam} n_iter={prob.n_iter} "
+         f"tol={prob.tol} c_batched={prob.c_batched}")
+    if gpu is None:
+        gpu = _gpu(prob)
+    if idx is None:
+        idx = np.arange(prob.B)
+    mu, nu, C = _subset(prob, idx)
+    iters = gpu["iters"][idx]
+    if prob.tol > 0:
+        free = oracle.forward(mu, nu, C, prob.lam, prob.n_iter, tol=prob.tol)
+        assert np.all(np.abs(free["iters"] - iters) <= 1), (free["iters"], iters)
+        ref = oracle.forward(mu, nu, C, prob.lam, prob.n_iter, n_iter_b=iters)
+    else:
+        assert np.all(iters == prob.n_iter)
+        ref = oracle.forward(mu, nu, C, prob.lam, prob.n_iter)
+    el = loss_rel_err(gpu["loss"][idx], ref["loss"])
+    ea, eb = gauge_fixed_errors(mu, nu, gpu["alpha"][idx], gpu["beta"][idx], ref["alpha"], ref["beta"])
+    dm = np.abs(gpu["marg_err"][idx] - ref["marg_err"])
+    _say(f"   loss rel {el:.2e}  alpha {ea:.2e}  beta {eb:.2e}  marg_err |d| max {dm.max():.2e} "
+         f"(ref max {ref['marg_err'].max():.2e})")
+    assert el <= LOSS_RTOL
+    assert ea <= pot_atol and eb <= pot_atol
+    assert np.all(dm <= merr_atol + merr_rtol * ref["marg_err"])
+    return gpu, ref
+
+
+def check_backward(prob, gpu, ref, idx=None, grad_C=False, seed=0):
+    if idx is None:
+        idx = np.arange(prob.B)
+    rng = np.random.default_rng(seed)
+    g = rng.uniform(0.5, 1.5, size=prob.B).astype(np.float32)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    out = sk.sinkhorn_backward(t(g), t(prob.mu), t(prob.nu), t(prob.C), prob.lam, t(gpu["alpha"]),
+                               t(gpu["beta"]), grad_C=grad_C)
+    torch.cuda.synchronize()
+    mu, nu, C = _subset(prob, idx)
+    r = oracle.backward(g[idx], mu, nu, C, prob.lam, ref["alpha"], ref["beta"], grad_C=grad_C and prob.c_batched)
+    gm, gn = out["grad_mu"].cpu().numpy()[idx], out["grad_nu"].cpu().numpy()[idx]
+    e1, e2 = rel_err_rows(gm, r["grad_mu"]), rel_err_rows(gn, r["grad_nu"])
+    _say(f"   grad_mu rel {e1:.2e}  grad_nu rel {e2:.2e}")
+    assert e1 <= GRAD_RTOL and e2 <= GRAD_RTOL
+    if grad_C:
+        gC = out["grad_C"].cpu().numpy()
+        if prob.c_batched:
+            e3 = rel_err_rows(gC[idx], r["grad_C"])
+        else:
+            assert len(idx) == prob.B, "shared grad_C sums the whole batch"
+            rs = oracle.backward(g, prob.mu, prob.nu, prob.C, prob.lam, ref["alpha"], ref["beta"], grad_C=True)
+            e3 = rel_err_rows(gC, rs["grad_C"])
+        _say(f"   grad_C rel {e3:.2e}")
+        assert e3 <= GRAD_RTOL
+
+
+# ---------------------------------------------------------------- workloads
+
+def test_tiny_full():
+    prob = workloads.make_config(1)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_label_subset_full_iterations():
+    prob = workloads.make_config(2, B=48)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_label_full_batch_sampled():
+    """The benchmark's launch: B=1024, d=100, 200 iterations; the oracle checks
+    a sample of the problems (each problem is independent)."""
+    prob = workloads.make_config(2)
+    gpu = _gpu(prob)
+    idx = np.array([0, 1, 257, 511, 512, 777, 1022, 1023])
+    gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx)
+    assert np.all(np.isfinite(gpu["loss"])) and np.all(gpu["marg_err"] < 1e-2)
+
+
+# ---------------------------------------------------------------- shapes and edge cases
+
+@pytest.mark.parametrize("d1,d2", [(16, 16), (17, 9), (32, 31), (33, 64), (65, 100), (104, 37), (105, 128),
+                                   (128, 128), (1, 7), (7, 1), (1, 1)])
+def test_shapes_every_template(d1, d2):
+    prob = workloads.random_problem(seed=d1 * 1000 + d2, B=5, d1=d1, d2=d2, lam=0.1, n_iter=40)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_zero_masses():
+    prob = workloads.random_problem(seed=7, B=6, d1=37, d2=100, lam=0.1, n_iter=60, zero_frac=0.25)
+    assert (prob.mu == 0).any() and (prob.nu == 0).any()
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+    gm = sk.sinkhorn_backward  # grads off the support are exactly 0
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    out = gm(t(np.ones(prob.B, np.float32)), t(prob.mu), t(prob.nu), t(prob.C), prob.lam, t(gpu["alpha"]),
+             t(gpu["beta"]))
+    assert np.all(out["grad_mu"].cpu().numpy()[prob.mu == 0] == 0)
+
+
+def test_per_sample_cost_resident():
+    prob = workloads.random_problem(seed=8, B=5, d1=20, d2=30, lam=0.05, n_iter=80, c_batched=True)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+@pytest.mark.parametrize("n_iter", [0, 1, 2])
+def test_few_iterations(n_iter):
+    prob = workloads.random_problem(seed=9, B=3, d1=12, d2=9, lam=0.2, n_iter=n_iter)
+    gpu, ref = check_forward(prob, merr_rtol=1e-3)
+    assert np.all(gpu["iters"] == n_iter)
+
+
+def test_single_sample_batch():
+    prob = workloads.random_problem(seed=10, B=1, d1=50, d2=70, lam=0.05, n_iter=100)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_early_stop_per_sample():
+    prob = workloads.random_problem(seed=11, B=6, d1=30, d2=40, lam=0.1, n_iter=400, tol=1e-4)
+    gpu, ref = check_forward(prob)
+    assert np.all(gpu["iters"] < 400) and len(set(gpu["iters"].tolist())) > 1
+    assert np.all(gpu["marg_err"] <= 1.5e-4)
+
+
+def test_unreachable_tol_runs_all_iterations():
+    prob = workloads.random_problem(seed=12, B=3, d1=20, d2=20, lam=0.01, n_iter=30, tol=1e-9)
+    gpu, ref = check_forward(prob)
+    assert np.all(gpu["iters"] == 30)
+
+
+def test_large_lambda_independent_coupling():
+    prob = workloads.random_problem(seed=13, B=4, d1=20, d2=25, lam=1e3, n_iter=5)
+    gpu, ref = check_forward(prob)
+    indep = np.einsum("bi,ij,bj->b", prob.mu.astype(np.float64), prob.C[0].astype(np.float64),
+                      prob.nu.astype(np.float64))
+    assert np.allclose(gpu["loss"], indep, rtol=1e-3)
+
+
+def test_small_lambda_1d_grid_w1():
+    """lambda = 1e-3 on a 1-D grid (C/lambda up to 1000): exercises the exact
+    logsumexp fallbacks; E^0 approaches the closed-form W1."""
+    prob = workloads.random_problem(seed=14, B=4, d1=100, d2=100, lam=1e-3, n_iter=300, cost="grid1d")
+    gpu, ref = check_forward(prob, merr_atol=1e-4)
+    x = np.linspace(0, 1, 100)
+    for k in range(prob.B):
+        w1 = np.abs(np.cumsum(prob.mu[k].astype(np.float64)) - np.cumsum(prob.nu[k].astype(np.float64)))[:-1].sum() * (x[1] - x[0])
+        assert gpu["loss"][k] == pytest.approx(w1, abs=1e-2 + 5 * gpu["marg_err"][k])
+
+
+def test_deterministic_bitwise():
+    prob = workloads.make_config(2, B=64)
+    a = _gpu(prob)
+    b = _gpu(prob)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_autograd_wrapper():
+    prob = workloads.random_problem(seed=15, B=4, d1=24, d2=24, lam=0.1, n_iter=50)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    mu = t(prob.mu).requires_grad_()
+    nu = t(prob.nu).requires_grad_()
+    C = t(prob.C[0]).requires_grad_()
+    loss, st = sk.sinkhorn_loss(mu, nu, C, prob.lam, prob.n_iter, return_state=True)
+    (loss * torch.arange(1, 5, device=DEV)).sum().backward()
+    ref = oracle.forward(prob.mu, prob.nu, prob.C, prob.lam, prob.n_iter)
+    g = oracle.backward(np.arange(1, 5), prob.mu, prob.nu, prob.C, prob.lam, ref["alpha"], ref["beta"], grad_C=True)
+    assert rel_err_rows(mu.grad.cpu().numpy(), g["grad_mu"]) <= GRAD_RTOL
+    assert rel_err_rows(nu.grad.cpu().numpy(), g["grad_nu"]) <= GRAD_RTOL
+    assert rel_err_rows(C.grad.cpu().numpy()[None], g["grad_C"]) <= GRAD_RTOL
