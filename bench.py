@@ -1,0 +1,224 @@
+"""Benchmark: batched log-domain Sinkhorn forward + backward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+One step = the whole hot path over one batch: sinkhorn_forward (all
+iterations, loss and marginal error) followed by sinkhorn_backward
+(grad_mu, grad_nu; plus grad_C for the point-cloud workload).  Inputs are
+synthetic (seeded, see workloads/) and resident in HBM before timing starts.
+
+Prints ONE JSON line.  value = cell-updates/s = sum_b d1*d2*iters_b per step
+divided by the step time.  The roofline object refers to the dominant kernel
+and is measured live with events on the stream the library launches on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+# v_exp_f32 issues a wave64 in 8 cycles per SIMD (half rate; measured 28.9 of
+# 32 per clock per CU in a pure-exp loop): 256 CUs x 4 SIMDs x 8 lanes/clk x 2.4 GHz
+PEAK_EXP_TS = 256 * 4 * 8 * 2.4e9 / 1e12
+
+WORKLOAD_NAMES = {
+    1: "tiny: B=4, d1=d2=10, shared 1-D squared cost, lambda=0.1, 100 iterations + backward",
+    2: "label: B=1024, d1=d2=100, shared squared-distance cost of 100 embeddings, lambda=0.05, "
+       "200 iterations + backward",
+    3: "image: B=256, d1=d2=784 (28x28), blob histograms, shared squared grid cost, lambda=0.01, "
+       "300 iterations + backward",
+    4: "grid: B=64, d1=d2=4096 (64x64), blob histograms, shared squared grid cost, lambda=1e-3, "
+       "500 iterations, tol=1e-6 + backward",
+    5: "clouds: B=32, d1=1024, d2=2048, per-sample squared-distance cost [32,1024,2048], lambda=0.05, "
+       "100 iterations + backward with grad_C",
+}
+
+
+def kernel_source_hash(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_1907_01729_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(profile_name, src_hash):
+    """HBM bytes per launch from a committed rocprofv3 --pmc summary, if it was
+    taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", profile_name)
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\s*(\{.*?\})\s*```", open(path).read(), re.S)
+    if not m:
+        return None
+    d = json.loads(m.group(1))
+    if d.get("source_hash") != src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(prob, grad_C):
+    """The fp64 oracle, as it stands, on the host cores: the same step
+    (forward + backward) on the whole batch."""
+    import oracle
+
+    t0 = time.perf_counter()
+    o = oracle.forward(prob.mu, prob.nu, prob.C, prob.lam, prob.n_iter, tol=prob.tol)
+    oracle.backward(np.ones(prob.B), prob.mu, prob.nu, prob.C, prob.lam, o["alpha"], o["beta"], grad_C=grad_C)
+    dt = time.perf_counter() - t0
+    cells = float(np.sum(o["iters"].astype(np.float64))) * prob.d1 * prob.d2
+    return dict(value=cells / dt, unit="cell-updates/s", cores=oracle.num_threads(), kind="oracle",
+                sample=f"whole batch of workload {prob.name} (B={prob.B}), one forward+backward, {dt:.2f} s")
+
+
+def cpu_baseline_sampled(prob, grad_C, n_samples):
+    import oracle
+    import workloads
+
+    idx = np.arange(n_samples)
+    C = prob.C[idx] if prob.c_batched else prob.C
+    sub = workloads.Problem(prob.name, prob.mu[idx], prob.nu[idx], C, prob.lam, prob.n_iter, prob.tol, grad_C)
+    r = cpu_baseline(sub, grad_C)
+    r["sample"] = (f"first {n_samples} of {prob.B} problems of workload {prob.name}, one forward+backward "
+                   f"({r['sample'].split(', ')[-1]})")
+    return r
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy 3 times (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (the batch is embarrassingly parallel; "
+              "multi-GPU sharding is design-only). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration:
+        n = 64 << 20  # 64 Mi floats = 256 MiB read + 256 MiB written per copy
+        x = torch.ones(n, device="cuda:0", dtype=torch.float32)
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "copies": 3}), flush=True)
+        return
+
+    import paper_1907_01729_amd as sk
+    import workloads
+
+    prob = workloads.make_config(args.config)
+    grad_C = bool(prob.grad_C)
+    dev = torch.device("cuda:0")
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    mu, nu, C = t(prob.mu), t(prob.nu), t(prob.C)
+    g = torch.ones(prob.B, device=dev, dtype=torch.float32)
+    ws = torch.empty((max(sk.sinkhorn_workspace_bytes(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.lam,
+                                                      prob.n_iter, prob.tol), 1),), device=dev, dtype=torch.uint8)
+    regime = sk.sinkhorn_regime(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.lam, prob.n_iter, prob.tol)
+
+    def step():
+        out = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter, prob.tol, workspace=ws)
+        sk.sinkhorn_backward(g, mu, nu, C, prob.lam, out["alpha"], out["beta"], grad_C=grad_C)
+        return out
+
+    for _ in range(args.warmup):
+        out = step()
+    torch.cuda.synchronize()
+    iters = out["iters"].cpu().numpy().astype(np.float64)
+    cells_per_step = float(iters.sum()) * prob.d1 * prob.d2
+
+    stream = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    e_all0, e_all1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e_all0.record(stream)
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        out = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter, prob.tol, workspace=ws)
+        ev[k][1].record(stream)
+        sk.sinkhorn_backward(g, mu, nu, C, prob.lam, out["alpha"], out["beta"], grad_C=grad_C)
+    e_all1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = e_all0.elapsed_time(e_all1) / args.steps
+    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    # Roofline of the dominant kernel.  Resident regime: the forward is ONE
+    # kernel; its algorithmic work is one exponential per cell per iteration
+    # plus one per cell for the first v-update and one for the loss epilogue.
+    cells = float(prob.B) * prob.d1 * prob.d2
+    exps = float(np.sum(iters + 2.0)) * prob.d1 * prob.d2
+    if regime == 1:
+        achieved = exps / (fwd_ms * 1e-3) / 1e12
+        src = kernel_source_hash(["sk_resident.hip", "sk_device.h"])
+        traffic = stored_traffic(f"sk_resident_kernel_{prob.name}_counters.md", src)
+        roof = dict(bound="alu", achieved=round(achieved, 4), peak=round(PEAK_EXP_TS, 4), unit="Texp/s",
+                    frac=round(achieved / PEAK_EXP_TS, 4), traffic=traffic,
+                    kernel="sk_resident_kernel", kernel_ms=round(fwd_ms, 5),
+                    work="exp2 per launch = (iters+2)*d1*d2 per problem")
+    else:
+        # Tiled regime: the forward is a sequence of sweeps (one pass over C
+        # each); per-sample C is HBM bound, shared C is exp bound.
+        if prob.c_batched:
+            nbytes = 4.0 * float(np.sum(iters + 2.0)) * prob.d1 * prob.d2
+            achieved = nbytes / (fwd_ms * 1e-3) / 1e9
+            roof = dict(bound="hbm", achieved=round(achieved, 2), peak=PEAK_HBM_GBS, unit="GB/s",
+                        frac=round(achieved / PEAK_HBM_GBS, 4), traffic=None, kernel="forward (sweeps)",
+                        kernel_ms=round(fwd_ms, 4), work="C bytes read per forward = 4*(iters+2)*d1*d2 per problem")
+        else:
+            achieved = exps / (fwd_ms * 1e-3) / 1e12
+            roof = dict(bound="alu", achieved=round(achieved, 4), peak=round(PEAK_EXP_TS, 4), unit="Texp/s",
+                        frac=round(achieved / PEAK_EXP_TS, 4), traffic=None, kernel="forward (sweeps)",
+                        kernel_ms=round(fwd_ms, 4), work="exp2 per forward = (iters+2)*d1*d2 per problem")
+
+    res = {
+        "metric": "Sinkhorn cell-updates/s (B*d1*d2*iters/s) fwd+bwd",
+        "value": cells_per_step / (ms_per_step * 1e-3),
+        "unit": "cell-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "wall_ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD_NAMES[args.config],
+            "B": prob.B, "d1": prob.d1, "d2": prob.d2, "lambda": prob.lam, "n_iter": prob.n_iter,
+            "tol": prob.tol, "c_batched": bool(prob.c_batched), "iters_done_mean": float(iters.mean()),
+            "regime": {1: "resident", 2: "tiled"}.get(regime, "?"),
+        },
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        if args.config in (1, 2):
+            res["cpu_baseline"] = cpu_baseline(prob, grad_C)
+        else:
+            res["cpu_baseline"] = cpu_baseline_sampled(prob, grad_C, {3: 16, 4: 1, 5: 2}[args.config])
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

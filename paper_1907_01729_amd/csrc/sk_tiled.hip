@@ -1,7 +1,449 @@
-// sk_tiled.hip -- placeholder until the tiled sweep lands.
+// sk_tiled.hip -- the forward for supports larger than the resident kernel takes.
+//
+// The batch is cut into (problem, row block) work-groups.  Per iteration ONE
+// sweep streams every cost row once: each wavefront takes whole rows, its 64
+// lanes cover the columns (coalesced), and for a row i it
+//   * builds e_ij = 2^(a_i + b_j + cl_ij) for all j and all-reduces the row sum
+//     over the wavefront (DPP / lane shuffles)           -> u-update of row i,
+//   * scales by f_i = 2^(a_i' - a_i) and accumulates the column sums of the
+//     updated plan in registers                           -> column partials.
+// (One exponential per cell per iteration; see the resident kernel for why the
+// current potential is a valid logsumexp shift.)  Column partials of a
+// work-group's wavefronts are combined in LDS, the row blocks' partials are
+// merged by a separate kernel in a fixed order (no float atomics), which also
+// performs the v-update and the column part of the marginal error.
+//
+// Launch sequence for n iterations:
+//   init                 a^0 = 0 on supp(mu), -inf off it; stop flags cleared
+//   col_exact + merge    v-update of iteration 1: online (max, sumexp) over i
+//                        per row block (Section 4's single-pass stabilised
+//                        logsumexp), merged across row blocks
+//   sweep(k), merge(k)   k = 1..n (no merge after the last sweep)
+//   sweep(stats), final  loss E^0 and marginal error of the returned iterate,
+//                        outputs in natural-log units
+// Early stop (tol > 0): sweep(k+1) sums the row-block and column-chunk error
+// partials of iterate k in a fixed order; every work-group of a problem takes
+// the same decision, and the first row block records K = k in the stop flag,
+// which later sweeps and merges honour.  Row-error partials are double
+// buffered so a decision never reads a partial being rewritten.
+#include "sk_device.h"
 #include "sk_internal.h"
 
 namespace sk {
-size_t tiled_workspace_bytes(int, int, int, int) { return 0; }
-hipError_t launch_tiled(const FwdArgs &, void *, hipStream_t) { return hipErrorNotSupported; }
+namespace {
+
+constexpr int kThreads = 256;  // 4 wavefronts per work-group
+constexpr int kWaves = kThreads / 64;
+constexpr float kPadCost = -1.0e30f;  // cost of cells beyond d2: plan entry 0, finite so 0*cl = 0
+constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the online max
+
+struct TiledArgs {
+    const float *mu, *nu, *C;
+    float *a;        // [B, d1] base-2 potentials (the alpha output buffer)
+    float *bbuf;     // [2][B, d2] base-2 column potentials, ping-pong by iteration parity
+    float *part;     // [2][R][B, d2] column partials (plane 1 only for the exact pass)
+    float *rowerr;   // [3][R][B] row-error partials: planes 0/1 by iteration parity, 2 for stats
+    float *lossp;    // [R][B] loss partials (stats)
+    float *colerr;   // [B][JC] column-error partials of the merge
+    int32_t *state;  // [B] 0 = running, K > 0 = stopped after iteration K
+    float *alpha_out, *beta_out, *loss_out, *merr_out;
+    int32_t *iters_out;
+    int B, d1, d2, R, RBS, JC, n_iter, c_batched;
+    float s, tol;
+};
+
+__device__ __forceinline__ size_t pidx(const TiledArgs &T, int plane, int r, int b, int j) {
+    return (((size_t)plane * T.R + r) * T.B + b) * (size_t)T.d2 + j;
+}
+
+// Work-group sum in a fixed order (deterministic); `red` holds kWaves floats.
+__device__ __forceinline__ float block_sum(float v, float *red) {
+    v = wave_sum(v);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += red[w];
+    return s;
+}
+
+__global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
+    const size_t n = (size_t)T.B * T.d1;
+    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < n; u += (size_t)gridDim.x * kThreads)
+        T.a[u] = T.mu[u] > 0.f ? 0.f : neg_inf();
+    const size_t m = (size_t)T.B * T.d2;
+    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < m; u += (size_t)gridDim.x * kThreads)
+        T.bbuf[u] = T.nu[u] > 0.f ? 0.f : neg_inf();  // b^0 (only used when n_iter == 0)
+    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < (size_t)T.B; u += (size_t)gridDim.x * kThreads)
+        T.state[u] = 0;
+}
+
+// v-update of iteration 1, per row block: online (max, sumexp) of
+// a^0_i + cl_ij over the block's rows for every column j (one thread per
+// (problem, column), reading cost rows coalesced across threads).
+__global__ __launch_bounds__(kThreads) void sk_tiled_col_exact(TiledArgs T) {
+    const int j = blockIdx.x * kThreads + threadIdx.x;
+    const int r = blockIdx.y, b = blockIdx.z;
+    if (j >= T.d2) return;
+    const int i0 = r * T.RBS, i1 = min(T.d1, i0 + T.RBS);
+    const float *Cb = T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0);
+    const float *mub = T.mu + (size_t)b * T.d1;
+    float m = kNegBig, s = 0.f;
+    for (int i = i0; i < i1; ++i) {
+        if (!(mub[i] > 0.f)) continue;  // a^0 = -inf: contributes nothing
+        const float x = -T.s * Cb[(size_t)i * T.d2 + j];
+        const float mn = fmaxf(m, x);
+        s = s * ex2(m - mn) + ex2(x - mn);
+        m = mn;
+    }
+    T.part[pidx(T, 0, r, b, j)] = m;
+    T.part[pidx(T, 1, r, b, j)] = s;
+}
+
+// Exact logsumexp (base 2) over all rows i of a_i + cl_ij for one column:
+// the fallback of the merge when the shifted column sum left [2^-64, 2^64].
+__device__ float col_lse_exact(const TiledArgs &T, int b, int j) {
+    const float *Cb = T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0);
+    const float *ab = T.a + (size_t)b * T.d1;
+    float m = neg_inf();
+    for (int i = 0; i < T.d1; ++i) m = fmaxf(m, ab[i] - T.s * Cb[(size_t)i * T.d2 + j]);
+    if (m == neg_inf()) return m;
+    float s = 0.f;
+    for (int i = 0; i < T.d1; ++i) s += ex2(ab[i] - T.s * Cb[(size_t)i * T.d2 + j] - m);
+    return m + lg2(s);
+}
+
+// Merge of the row blocks' column partials (fixed order) and v-update.
+// EXACT: partials are (max, sumexp) pairs of the first v-update.
+// Otherwise: partials are the column sums of the plan after sweep k; this also
+// yields the column part of iterate k's marginal error.
+template <bool EXACT>
+__global__ __launch_bounds__(kThreads) void sk_tiled_merge(TiledArgs T, int k) {
+    __shared__ float red[kWaves];
+    const int j = blockIdx.x * kThreads + threadIdx.x;
+    const int b = blockIdx.y;
+    if (!EXACT && T.state[b] != 0) return;  // block-uniform
+    float err = 0.f;
+    if (j < T.d2) {
+        const float nuj = T.nu[(size_t)b * T.d2 + j];
+        float bnew = neg_inf();
+        if (EXACT) {
+            float M = kNegBig;
+            for (int r = 0; r < T.R; ++r) M = fmaxf(M, T.part[pidx(T, 0, r, b, j)]);
+            float S = 0.f;
+            for (int r = 0; r < T.R; ++r) S += T.part[pidx(T, 1, r, b, j)] * ex2(T.part[pidx(T, 0, r, b, j)] - M);
+            if (nuj > 0.f) bnew = log2f(nuj) - (M + lg2(S));
+            T.bbuf[(size_t)1 * T.B * T.d2 + (size_t)b * T.d2 + j] = bnew;
+        } else {
+            float cs = 0.f;
+            for (int r = 0; r < T.R; ++r) cs += T.part[pidx(T, 0, r, b, j)];
+            err = fabsf(cs - nuj);
+            if (nuj > 0.f) {
+                const float bold = T.bbuf[(size_t)(k & 1) * T.B * T.d2 + (size_t)b * T.d2 + j];
+                if (cs >= kSumLo && cs <= kSumHi)
+                    bnew = bold + log2f(nuj) - lg2(cs);
+                else
+                    bnew = log2f(nuj) - col_lse_exact(T, b, j);
+            }
+            T.bbuf[(size_t)((k + 1) & 1) * T.B * T.d2 + (size_t)b * T.d2 + j] = bnew;
+        }
+    }
+    if (!EXACT) {
+        err = block_sum(err, red);
+        if (threadIdx.x == 0) T.colerr[(size_t)b * T.JC + blockIdx.x] = err;
+    }
+}
+
+// The sweep.  Work-group (row block r, problem b); wavefront w takes rows
+// i0 + w, i0 + w + 4, ...; lane l owns columns j = l + 64 c, c < NCW.
+// STATS: no update; plan of the current (a, b) with loss partials.
+template <int NCW, bool STATS, bool BATCHED>
+__global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
+    extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
+    __shared__ float scal[2 * kWaves];
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int d1 = T.d1, d2 = T.d2;
+
+    int st = T.state[b];
+    if (!STATS) {
+        if (st != 0) return;
+        if (T.tol > 0.f && k >= 2) {
+            // marginal error of iterate k-1: row blocks then column chunks, fixed order
+            const float *re = T.rowerr + (size_t)((k - 1) & 1) * T.R * T.B;
+            float err = 0.f;
+            for (int q = 0; q < T.R; ++q) err += re[(size_t)q * T.B + b];
+            for (int c = 0; c < T.JC; ++c) err += T.colerr[(size_t)b * T.JC + c];
+            if (err <= T.tol) {
+                if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
+                return;
+            }
+        }
+    }
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * d2 + (size_t)b * d2;
+    const float *Cb = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0);
+    float *ab = T.a + (size_t)b * d1;
+    const float *mub = T.mu + (size_t)b * d1;
+
+    float bv[NCW], colpart[NCW];
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const int j = lane + 64 * c;
+        bv[c] = j < d2 ? bsrc[j] : 0.f;
+        colpart[c] = 0.f;
+    }
+    float rowerr = 0.f, losspart = 0.f;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    for (int i = i0 + w; i < i1; i += kWaves) {
+        const float ai = ab[i];
+        const float mui = mub[i];
+        const float *Crow = Cb + (size_t)i * d2;
+        float e[NCW];
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) {
+            const int j = lane + 64 * c;
+            // a per-sample cost is streamed once per iteration (keep it out of
+            // the caches); a shared cost is re-read by the other problems' groups
+            const float cv = j < d2 ? (BATCHED ? __builtin_nontemporal_load(Crow + j) : Crow[j]) : 0.f;
+            e[c] = j < d2 ? -T.s * cv : kPadCost;
+        }
+        float part = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) {
+            const float cl = e[c];
+            const float v = ex2((ai + bv[c]) + cl);
+            if (STATS) losspart = __builtin_fmaf(v, cl, losspart);
+            e[c] = v;
+            part += v;
+        }
+        const float rs = wave_sum(part);
+        if (STATS) {
+            if (mui > 0.f) rowerr += fabsf(rs - mui);
+#pragma unroll
+            for (int c = 0; c < NCW; ++c) colpart[c] += e[c];
+        } else if (mui > 0.f) {
+            const float lmu = log2f(mui);
+            float an, f;
+            if (rs >= kSumLo && rs <= kSumHi) {
+                an = ai + lmu - lg2(rs);
+                f = ex2(an - ai);
+                rowerr += fabsf(f * rs - mui);
+            } else {
+                // Exact u-update of this row (max, then sum), plan entries
+                // rebuilt from the new potential.
+                float m = neg_inf();
+#pragma unroll
+                for (int c = 0; c < NCW; ++c) {
+                    const int j = lane + 64 * c;
+                    const float cl = j < d2 ? -T.s * Crow[j] : kPadCost;
+                    m = fmaxf(m, bv[c] + cl);
+                }
+                m = wave_max(m);
+                float s2 = 0.f;
+#pragma unroll
+                for (int c = 0; c < NCW; ++c) {
+                    const int j = lane + 64 * c;
+                    const float cl = j < d2 ? -T.s * Crow[j] : kPadCost;
+                    s2 += ex2(bv[c] + cl - m);
+                }
+                s2 = wave_sum(s2);
+                an = lmu - (m + lg2(s2));
+                float p2 = 0.f;
+#pragma unroll
+                for (int c = 0; c < NCW; ++c) {
+                    const int j = lane + 64 * c;
+                    const float cl = j < d2 ? -T.s * Crow[j] : kPadCost;
+                    e[c] = ex2((an + bv[c]) + cl);
+                    p2 += e[c];
+                }
+                p2 = wave_sum(p2);
+                f = 1.f;
+                rowerr += fabsf(p2 - mui);
+            }
+#pragma unroll
+            for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[c], f, colpart[c]);
+            if (lane == 0) ab[i] = an;
+        }
+    }
+
+    // Combine the wavefronts' partials in LDS, fixed order, and store.
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) lds[w * NCW * 64 + c * 64 + lane] = colpart[c];
+    // rowerr is wavefront-uniform (built from all-reduced sums); losspart is per lane
+    const float lw = STATS ? wave_sum(losspart) : 0.f;
+    if (lane == 0) {
+        scal[w] = rowerr;
+        scal[kWaves + w] = lw;
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < d2; j += kThreads) {
+        float s = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) s += lds[q * NCW * 64 + j];
+        T.part[pidx(T, 0, r, b, j)] = s;
+    }
+    if (threadIdx.x == 0) {
+        float re = 0.f, lo = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) {
+            re += scal[q];
+            lo += scal[kWaves + q];
+        }
+        const int plane = STATS ? 2 : (k & 1);
+        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
+        if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
+    }
+}
+
+// Outputs of the returned iterate: marginal error, E^0, natural-log potentials.
+__global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
+    __shared__ float red[kWaves];
+    const int b = blockIdx.x;
+    const int st = T.state[b];
+    const int K = st ? st : T.n_iter;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2 + (size_t)b * T.d2;
+    float colerr = 0.f;
+    for (int j = threadIdx.x; j < T.d2; j += kThreads) {
+        float cs = 0.f;
+        for (int r = 0; r < T.R; ++r) cs += T.part[pidx(T, 0, r, b, j)];
+        colerr += fabsf(cs - T.nu[(size_t)b * T.d2 + j]);
+        T.beta_out[(size_t)b * T.d2 + j] = bsrc[j] * kLn2;
+    }
+    for (int i = threadIdx.x; i < T.d1; i += kThreads) {
+        const size_t u = (size_t)b * T.d1 + i;
+        T.alpha_out[u] = T.a[u] * kLn2;
+    }
+    colerr = block_sum(colerr, red);
+    if (threadIdx.x == 0) {
+        float re = 0.f, lo = 0.f;
+        for (int r = 0; r < T.R; ++r) {
+            re += T.rowerr[((size_t)2 * T.R + r) * T.B + b];
+            lo += T.lossp[(size_t)r * T.B + b];
+        }
+        T.loss_out[b] = -lo / T.s;
+        T.merr_out[b] = re + colerr;
+        T.iters_out[b] = K;
+    }
+}
+
+// Row blocks: enough work-groups to fill the chip (>= ~2048 wavefronts), rows
+// per block a multiple of the wavefronts per group.
+void row_blocks(int B, int d1, int *R, int *RBS) {
+    int want = (2048 / kWaves + B - 1) / (B > 0 ? B : 1);
+    int maxR = (d1 + kWaves - 1) / kWaves;
+    int r = want < 1 ? 1 : (want > maxR ? maxR : want);
+    int rbs = (d1 + r - 1) / r;
+    rbs = (rbs + kWaves - 1) / kWaves * kWaves;
+    *RBS = rbs;
+    *R = (d1 + rbs - 1) / rbs;
+}
+
+struct Layout {
+    size_t bbuf, part, rowerr, lossp, colerr, state, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Layout layout(int B, int d1, int d2, int *R_out, int *RBS_out, int *JC_out) {
+    int R, RBS;
+    row_blocks(B, d1, &R, &RBS);
+    const int JC = (d2 + kThreads - 1) / kThreads;
+    Layout L;
+    size_t off = 0;
+    L.bbuf = off;
+    off = align256(off + sizeof(float) * 2 * (size_t)B * d2);
+    L.part = off;
+    off = align256(off + sizeof(float) * 2 * (size_t)R * B * d2);
+    L.rowerr = off;
+    off = align256(off + sizeof(float) * 3 * (size_t)R * B);
+    L.lossp = off;
+    off = align256(off + sizeof(float) * (size_t)R * B);
+    L.colerr = off;
+    off = align256(off + sizeof(float) * (size_t)B * JC);
+    L.state = off;
+    off = align256(off + sizeof(int32_t) * (size_t)B);
+    L.total = off;
+    if (R_out) *R_out = R;
+    if (RBS_out) *RBS_out = RBS;
+    if (JC_out) *JC_out = JC;
+    return L;
+}
+
+template <int NCW, bool BATCHED>
+hipError_t run(const TiledArgs &T, hipStream_t st) {
+    const size_t lds = sizeof(float) * kWaves * NCW * 64;
+    const dim3 blk(kThreads);
+    hipLaunchKernelGGL(sk_tiled_init, dim3(512), blk, 0, st, T);
+    if (T.n_iter > 0) {
+        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), blk, 0, st, T);
+        hipLaunchKernelGGL(sk_tiled_merge<true>, dim3(T.JC, T.B), blk, 0, st, T, 0);
+        for (int k = 1; k <= T.n_iter; ++k) {
+            hipLaunchKernelGGL((sk_tiled_sweep<NCW, false, BATCHED>), dim3(T.R, T.B), blk, lds, st, T, k);
+            if (k < T.n_iter) hipLaunchKernelGGL(sk_tiled_merge<false>, dim3(T.JC, T.B), blk, 0, st, T, k);
+        }
+    }
+    hipLaunchKernelGGL((sk_tiled_sweep<NCW, true, BATCHED>), dim3(T.R, T.B), blk, lds, st, T, 0);
+    hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), blk, 0, st, T);
+    return hipGetLastError();
+}
+
+template <bool BATCHED>
+hipError_t dispatch(const TiledArgs &T, int ncw, hipStream_t st) {
+    if (ncw <= 4) return run<4, BATCHED>(T, st);
+    if (ncw <= 8) return run<8, BATCHED>(T, st);
+    if (ncw <= 13) return run<13, BATCHED>(T, st);
+    if (ncw <= 16) return run<16, BATCHED>(T, st);
+    if (ncw <= 32) return run<32, BATCHED>(T, st);
+    return run<64, BATCHED>(T, st);
+}
+
+}  // namespace
+
+size_t tiled_workspace_bytes(int B, int d1, int d2, int /*c_batched*/) {
+    return layout(B, d1, d2, nullptr, nullptr, nullptr).total;
+}
+
+bool tiled_fits(int B, int d1, int d2) {
+    int R, RBS;
+    row_blocks(B, d1, &R, &RBS);
+    return d2 <= kTiledMaxD2 && B <= 65535 && R <= 65535;
+}
+
+hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
+    TiledArgs T;
+    int R, RBS, JC;
+    const Layout L = layout(a.B, a.d1, a.d2, &R, &RBS, &JC);
+    char *base = static_cast<char *>(ws);
+    T.mu = a.mu;
+    T.nu = a.nu;
+    T.C = a.C;
+    T.a = a.alpha;
+    T.bbuf = reinterpret_cast<float *>(base + L.bbuf);
+    T.part = reinterpret_cast<float *>(base + L.part);
+    T.rowerr = reinterpret_cast<float *>(base + L.rowerr);
+    T.lossp = reinterpret_cast<float *>(base + L.lossp);
+    T.colerr = reinterpret_cast<float *>(base + L.colerr);
+    T.state = reinterpret_cast<int32_t *>(base + L.state);
+    T.alpha_out = a.alpha;
+    T.beta_out = a.beta;
+    T.loss_out = a.loss;
+    T.merr_out = a.marg_err;
+    T.iters_out = a.iters;
+    T.B = a.B;
+    T.d1 = a.d1;
+    T.d2 = a.d2;
+    T.R = R;
+    T.RBS = RBS;
+    T.JC = JC;
+    T.n_iter = a.n_iter;
+    T.c_batched = a.c_batched;
+    T.s = a.s;
+    T.tol = a.tol;
+    const int ncw = (a.d2 + 63) / 64;
+    if (a.c_batched) return dispatch<true>(T, ncw, st);
+    return dispatch<false>(T, ncw, st);
+}
+
 }  // namespace sk

@@ -52,6 +52,7 @@ def test_regime_and_workspace_queries():
     assert sk.sinkhorn_regime(4, 10, 10, 0, lam=0.0) == 0
     assert sk.sinkhorn_workspace_bytes(4, 10, 10, 0, 0.1, 100) == 0
     assert sk.sinkhorn_workspace_bytes(256, 784, 784, 0, 0.01, 300) > 0
+    assert sk.sinkhorn_regime(4, 200, 4097, 0) == 0  # no kernel takes d2 > 4096 beyond the resident sizes
     assert sk.sinkhorn_workspace_bytes(-1, 784, 784, 0, 0.01, 300) == 0
 
 
