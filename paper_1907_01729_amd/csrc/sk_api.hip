@@ -15,7 +15,7 @@ sk_status check_problem(const sk_problem *p) {
     if (p->c_batched != 0 && p->c_batched != 1) return SK_ERR_SHAPE;
     const int64_t cells = (int64_t)p->d1 * p->d2;
     if (cells > (int64_t(1) << 40) || (int64_t)p->B * cells > (int64_t(1) << 46)) return SK_ERR_SHAPE;
-    if (!sk::resident_fits(p->d1, p->d2) && !sk::tiled_fits(p->B, p->d1, p->d2)) return SK_ERR_SHAPE;
+    if (!sk::resident_fits(p->d1, p->d2) && !sk::tiled_fits(p->B, p->d1, p->d2, p->c_batched)) return SK_ERR_SHAPE;
     if (!(p->lambda > 0.f) || !isfinite(p->lambda)) return SK_ERR_LAMBDA;
     if (p->n_iter < 0 || !isfinite(p->tol)) return SK_ERR_ITERS;
     return SK_OK;

@@ -51,21 +51,51 @@ __device__ __forceinline__ float max_q(float v) {
     v = fmaxf(v, dpp<kHalfMirror>(v));
     return v;
 }
+// Exchange across DPP rows with gfx950's v_permlane{16,32}_swap: with both
+// operands = x, lane l gets the pair (x[l & ~16], x[l | 16]) (resp. 32), the
+// same ordered pair on lane l and lane l ^ 16 (resp. 32), so one swap plus one
+// add is an all-reduce step whose result is bit-identical on both lanes.
+struct LanePair {
+    float lo, hi;
+};
+__device__ __forceinline__ LanePair swap16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ LanePair swap32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
 // All-reduce over the 8 lanes q, q+8, ..., q+56 (same lane & 7).
 __device__ __forceinline__ float sum_p(float v) {
     v += dpp<kRowRor8>(v);
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
-    return v;
+    LanePair a = swap16(v);
+    v = a.lo + a.hi;
+    LanePair b = swap32(v);
+    return b.lo + b.hi;
 }
 __device__ __forceinline__ float max_p(float v) {
     v = fmaxf(v, dpp<kRowRor8>(v));
-    v = fmaxf(v, __shfl_xor(v, 16));
-    v = fmaxf(v, __shfl_xor(v, 32));
-    return v;
+    LanePair a = swap16(v);
+    v = fmaxf(a.lo, a.hi);
+    LanePair b = swap32(v);
+    return fmaxf(b.lo, b.hi);
 }
 // Whole-wavefront all-reduce (bit-identical on every lane).
 __device__ __forceinline__ float wave_sum(float v) { return sum_p(sum_q(v)); }
 __device__ __forceinline__ float wave_max(float v) { return max_p(max_q(v)); }
+
+// Pairwise (tree) sum of a register array: log-depth dependency chain instead
+// of a serial one, so that few wavefronts per SIMD still keep the VALU busy.
+template <int N>
+__device__ __forceinline__ float tree_sum(const float *v) {
+    if constexpr (N == 1) {
+        return v[0];
+    } else {
+        constexpr int L = N / 2;
+        return tree_sum<L>(v) + tree_sum<N - L>(v + L);
+    }
+}
 
 }  // namespace sk

@@ -36,7 +36,7 @@ hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
 
 // The tiled sweep keeps a whole cost row in one wavefront's registers.
 constexpr int kTiledMaxD2 = 4096;
-bool tiled_fits(int B, int d1, int d2);
+bool tiled_fits(int B, int d1, int d2, int c_batched);
 size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched);
 hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);
 

@@ -34,6 +34,7 @@ namespace {
 
 constexpr int kThreads = 256;  // 4 wavefronts per work-group
 constexpr int kWaves = kThreads / 64;
+constexpr int kMergeThreads = 64;  // merge: one wavefront per (problem, 64 columns)
 constexpr float kPadCost = -1.0e30f;  // cost of cells beyond d2: plan entry 0, finite so 0*cl = 0
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the online max
 
@@ -82,8 +83,8 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
 // v-update of iteration 1, per row block: online (max, sumexp) of
 // a^0_i + cl_ij over the block's rows for every column j (one thread per
 // (problem, column), reading cost rows coalesced across threads).
-__global__ __launch_bounds__(kThreads) void sk_tiled_col_exact(TiledArgs T) {
-    const int j = blockIdx.x * kThreads + threadIdx.x;
+__global__ __launch_bounds__(kMergeThreads) void sk_tiled_col_exact(TiledArgs T) {
+    const int j = blockIdx.x * kMergeThreads + threadIdx.x;
     const int r = blockIdx.y, b = blockIdx.z;
     if (j >= T.d2) return;
     const int i0 = r * T.RBS, i1 = min(T.d1, i0 + T.RBS);
@@ -119,9 +120,8 @@ __device__ float col_lse_exact(const TiledArgs &T, int b, int j) {
 // Otherwise: partials are the column sums of the plan after sweep k; this also
 // yields the column part of iterate k's marginal error.
 template <bool EXACT>
-__global__ __launch_bounds__(kThreads) void sk_tiled_merge(TiledArgs T, int k) {
-    __shared__ float red[kWaves];
-    const int j = blockIdx.x * kThreads + threadIdx.x;
+__global__ __launch_bounds__(kMergeThreads) void sk_tiled_merge(TiledArgs T, int k) {
+    const int j = blockIdx.x * kMergeThreads + threadIdx.x;
     const int b = blockIdx.y;
     if (!EXACT && T.state[b] != 0) return;  // block-uniform
     float err = 0.f;
@@ -150,14 +150,101 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_merge(TiledArgs T, int k) {
         }
     }
     if (!EXACT) {
-        err = block_sum(err, red);
+        err = wave_sum(err);
         if (threadIdx.x == 0) T.colerr[(size_t)b * T.JC + blockIdx.x] = err;
     }
 }
 
-// The sweep.  Work-group (row block r, problem b); wavefront w takes rows
-// i0 + w, i0 + w + 4, ...; lane l owns columns j = l + 64 c, c < NCW.
-// STATS: no update; plan of the current (a, b) with loss partials.
+// Cost of this lane's columns j = lane + 64 c of one row, read from global
+// memory and scaled on the fly (kPadCost beyond d2).  A per-sample cost is
+// streamed once per iteration, so it bypasses the caches.
+template <bool BATCHED>
+struct GlobalCost {
+    const float *row;
+    int lane, d2;
+    float s;
+    __device__ __forceinline__ float operator()(int c) const {
+        const int j = lane + 64 * c;
+        if (j >= d2) return kPadCost;
+        return -s * (BATCHED ? __builtin_nontemporal_load(row + j) : row[j]);
+    }
+};
+// The same from a row staged (already scaled and padded) in LDS.
+struct LdsCost {
+    const float *row;  // already offset by lane
+    __device__ __forceinline__ float operator()(int c) const { return row[64 * c]; }
+};
+
+// One cost row i of one problem in one wavefront: e_j = 2^(a_i + b_j + cl_ij),
+// row sum by wavefront all-reduce, u-update of a_i, and the column sums of the
+// updated plan accumulated into colpart.  STATS: the plan of the current (a, b)
+// without update, with sum P*cl.  rowerr (wavefront-uniform) gathers the rows'
+// marginal error.
+template <int NCW, bool STATS, class Cost>
+__device__ __forceinline__ void row_step(const Cost &cost, float ai, float mui, float *a_row,
+                                         const float (&bv)[NCW], float (&colpart)[NCW], float &rowerr,
+                                         float &losspart, int lane) {
+    float e[NCW];
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) e[c] = cost(c);
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const float cl = e[c];
+        const float v = ex2((ai + bv[c]) + cl);
+        if (STATS) losspart = __builtin_fmaf(v, cl, losspart);
+        e[c] = v;
+    }
+    const float rs = wave_sum(tree_sum<NCW>(e));
+    if (STATS) {
+        if (mui > 0.f) rowerr += fabsf(rs - mui);
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) colpart[c] += e[c];
+        return;
+    }
+    if (!(mui > 0.f)) return;  // zero-mass row: a_i = -inf, all its entries 0
+    const float lmu = log2f(mui);
+    float an, f;
+    if (rs >= kSumLo && rs <= kSumHi) {
+        an = ai + lmu - lg2(rs);
+        f = ex2(an - ai);
+        rowerr += fabsf(f * rs - mui);
+    } else {
+        // Exact u-update of this row (max, then sum), plan entries rebuilt
+        // from the new potential.
+        float m = neg_inf();
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) m = fmaxf(m, bv[c] + cost(c));
+        m = wave_max(m);
+        float s2 = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) s2 += ex2(bv[c] + cost(c) - m);
+        s2 = wave_sum(s2);
+        an = lmu - (m + lg2(s2));
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) e[c] = ex2((an + bv[c]) + cost(c));
+        f = 1.f;
+        rowerr += fabsf(wave_sum(tree_sum<NCW>(e)) - mui);
+    }
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[c], f, colpart[c]);
+    if (lane == 0) *a_row = an;
+}
+
+// Early-stop test of problem b before sweep k (k >= 2): the marginal error of
+// iterate k-1 from the row-block and column-chunk partials, fixed order.
+__device__ __forceinline__ bool stop_before(const TiledArgs &T, int b, int k) {
+    if (!(T.tol > 0.f) || k < 2) return false;
+    const float *re = T.rowerr + (size_t)((k - 1) & 1) * T.R * T.B;
+    float err = 0.f;
+    for (int q = 0; q < T.R; ++q) err += re[(size_t)q * T.B + b];
+    for (int c = 0; c < T.JC; ++c) err += T.colerr[(size_t)b * T.JC + c];
+    return err <= T.tol;
+}
+
+// Sweep, one problem per work-group (per-sample costs, or tiny batches).
+// Work-group (row block r, problem b); wavefront w takes rows i0 + w,
+// i0 + w + 4, ...; lane l owns columns j = l + 64 c, c < NCW.  The
+// wavefronts' column partials are combined in LDS in a fixed order.
 template <int NCW, bool STATS, bool BATCHED>
 __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
     extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
@@ -166,19 +253,12 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int d1 = T.d1, d2 = T.d2;
 
-    int st = T.state[b];
+    const int st = T.state[b];
     if (!STATS) {
         if (st != 0) return;
-        if (T.tol > 0.f && k >= 2) {
-            // marginal error of iterate k-1: row blocks then column chunks, fixed order
-            const float *re = T.rowerr + (size_t)((k - 1) & 1) * T.R * T.B;
-            float err = 0.f;
-            for (int q = 0; q < T.R; ++q) err += re[(size_t)q * T.B + b];
-            for (int c = 0; c < T.JC; ++c) err += T.colerr[(size_t)b * T.JC + c];
-            if (err <= T.tol) {
-                if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
-                return;
-            }
+        if (stop_before(T, b, k)) {
+            if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
+            return;
         }
     }
     const int K = STATS ? (st ? st : T.n_iter) : k;
@@ -197,75 +277,8 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
     float rowerr = 0.f, losspart = 0.f;
     const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
     for (int i = i0 + w; i < i1; i += kWaves) {
-        const float ai = ab[i];
-        const float mui = mub[i];
-        const float *Crow = Cb + (size_t)i * d2;
-        float e[NCW];
-#pragma unroll
-        for (int c = 0; c < NCW; ++c) {
-            const int j = lane + 64 * c;
-            // a per-sample cost is streamed once per iteration (keep it out of
-            // the caches); a shared cost is re-read by the other problems' groups
-            const float cv = j < d2 ? (BATCHED ? __builtin_nontemporal_load(Crow + j) : Crow[j]) : 0.f;
-            e[c] = j < d2 ? -T.s * cv : kPadCost;
-        }
-        float part = 0.f;
-#pragma unroll
-        for (int c = 0; c < NCW; ++c) {
-            const float cl = e[c];
-            const float v = ex2((ai + bv[c]) + cl);
-            if (STATS) losspart = __builtin_fmaf(v, cl, losspart);
-            e[c] = v;
-            part += v;
-        }
-        const float rs = wave_sum(part);
-        if (STATS) {
-            if (mui > 0.f) rowerr += fabsf(rs - mui);
-#pragma unroll
-            for (int c = 0; c < NCW; ++c) colpart[c] += e[c];
-        } else if (mui > 0.f) {
-            const float lmu = log2f(mui);
-            float an, f;
-            if (rs >= kSumLo && rs <= kSumHi) {
-                an = ai + lmu - lg2(rs);
-                f = ex2(an - ai);
-                rowerr += fabsf(f * rs - mui);
-            } else {
-                // Exact u-update of this row (max, then sum), plan entries
-                // rebuilt from the new potential.
-                float m = neg_inf();
-#pragma unroll
-                for (int c = 0; c < NCW; ++c) {
-                    const int j = lane + 64 * c;
-                    const float cl = j < d2 ? -T.s * Crow[j] : kPadCost;
-                    m = fmaxf(m, bv[c] + cl);
-                }
-                m = wave_max(m);
-                float s2 = 0.f;
-#pragma unroll
-                for (int c = 0; c < NCW; ++c) {
-                    const int j = lane + 64 * c;
-                    const float cl = j < d2 ? -T.s * Crow[j] : kPadCost;
-                    s2 += ex2(bv[c] + cl - m);
-                }
-                s2 = wave_sum(s2);
-                an = lmu - (m + lg2(s2));
-                float p2 = 0.f;
-#pragma unroll
-                for (int c = 0; c < NCW; ++c) {
-                    const int j = lane + 64 * c;
-                    const float cl = j < d2 ? -T.s * Crow[j] : kPadCost;
-                    e[c] = ex2((an + bv[c]) + cl);
-                    p2 += e[c];
-                }
-                p2 = wave_sum(p2);
-                f = 1.f;
-                rowerr += fabsf(p2 - mui);
-            }
-#pragma unroll
-            for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[c], f, colpart[c]);
-            if (lane == 0) ab[i] = an;
-        }
+        const GlobalCost<BATCHED> cost{Cb + (size_t)i * d2, lane, d2, T.s};
+        row_step<NCW, STATS>(cost, ab[i], mub[i], ab + i, bv, colpart, rowerr, losspart, lane);
     }
 
     // Combine the wavefronts' partials in LDS, fixed order, and store.
@@ -294,6 +307,208 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
         const int plane = STATS ? 2 : (k & 1);
         T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
         if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
+    }
+}
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// Cost of a row held in registers (raw C, 4 consecutive columns per float4:
+// element cc is column j = 4 lane + 256 (cc / 4) + cc % 4), scaled on use.
+template <int NCW>
+struct RegCost {
+    const float *v;
+    int lane, d2;
+    float s;
+    __device__ __forceinline__ float operator()(int cc) const {
+        const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
+        return j < d2 ? -s * v[cc] : kPadCost;
+    }
+};
+
+// Sweep for per-sample costs (each C_b read once per iteration, HBM bound):
+// as sk_tiled_sweep, but every lane streams 128-bit non-temporal loads of 4
+// consecutive columns and the next row of the wavefront is in flight while
+// the current one is computed.  Needs d2 % 4 == 0 (16-byte aligned rows).
+template <int NC4, bool STATS>
+__global__ __launch_bounds__(kThreads) void sk_tiled_sweep_stream(TiledArgs T, int k) {
+    constexpr int NCW = 4 * NC4;
+    extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
+    __shared__ float scal[2 * kWaves];
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int d1 = T.d1, d2 = T.d2;
+
+    const int st = T.state[b];
+    if (!STATS) {
+        if (st != 0) return;
+        if (stop_before(T, b, k)) {
+            if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
+            return;
+        }
+    }
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * d2 + (size_t)b * d2;
+    const float *Cb = T.C + (size_t)b * d1 * d2;
+    float *ab = T.a + (size_t)b * d1;
+    const float *mub = T.mu + (size_t)b * d1;
+
+    float bv[NCW], colpart[NCW];
+#pragma unroll
+    for (int cc = 0; cc < NCW; ++cc) {
+        const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
+        bv[cc] = j < d2 ? bsrc[j] : 0.f;
+        colpart[cc] = 0.f;
+    }
+    auto load_row = [&](float (&dst)[NCW], int i) {
+        const f4v *row = reinterpret_cast<const f4v *>(Cb + (size_t)i * d2);
+#pragma unroll
+        for (int c = 0; c < NC4; ++c) {
+            const int j0 = 4 * lane + 256 * c;
+            f4v v = {0.f, 0.f, 0.f, 0.f};
+            if (j0 < d2) v = __builtin_nontemporal_load(row + (j0 >> 2));
+            dst[4 * c + 0] = v.x;
+            dst[4 * c + 1] = v.y;
+            dst[4 * c + 2] = v.z;
+            dst[4 * c + 3] = v.w;
+        }
+    };
+    float rowerr = 0.f, losspart = 0.f;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    float cur[NCW], nxt[NCW];
+    int i = i0 + w;
+    if (i < i1) load_row(cur, i);
+    for (; i < i1; i += kWaves) {
+        if (i + kWaves < i1) load_row(nxt, i + kWaves);  // in flight during this row
+        const RegCost<NCW> cost{cur, lane, d2, T.s};
+        row_step<NCW, STATS>(cost, ab[i], mub[i], ab + i, bv, colpart, rowerr, losspart, lane);
+#pragma unroll
+        for (int cc = 0; cc < NCW; ++cc) cur[cc] = nxt[cc];
+    }
+
+#pragma unroll
+    for (int cc = 0; cc < NCW; ++cc) {
+        const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
+        lds[w * NCW * 64 + j] = colpart[cc];
+    }
+    const float lw = STATS ? wave_sum(losspart) : 0.f;
+    if (lane == 0) {
+        scal[w] = rowerr;
+        scal[kWaves + w] = lw;
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < d2; j += kThreads) {
+        float s = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) s += lds[q * NCW * 64 + j];
+        T.part[pidx(T, 0, r, b, j)] = s;
+    }
+    if (threadIdx.x == 0) {
+        float re = 0.f, lo = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) {
+            re += scal[q];
+            lo += scal[kWaves + q];
+        }
+        const int plane = STATS ? 2 : (k & 1);
+        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
+        if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
+    }
+}
+
+// Sweep for a cost shared by the batch (Section 4's setting): a work-group of
+// W wavefronts = W problems of group g walks the rows of row block r; chunks
+// of RS cost rows are staged once in LDS (scaled, padded, double-buffered) and
+// read by all W wavefronts, so each cost element leaves L2 once per W
+// problems.  Work-groups of the same row block share an XCD (block index
+// r + R g with R a multiple of 8), so the row block leaves HBM once.
+template <int NCW, int W, bool STATS>
+__global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int k) {
+    constexpr int D2P = NCW * 64;              // padded row length in LDS
+    constexpr int RS = (64 / NCW) < 8 ? (64 / NCW) : 8;  // rows per staged chunk (2 x RS x D2P <= 32 KB)
+    constexpr int NT = 64 * W;
+    constexpr int NLD = (RS * D2P + NT - 1) / NT;  // staging loads per thread
+    extern __shared__ float lds[];                 // [2][RS][D2P]
+    const int r = blockIdx.x, g = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int d1 = T.d1, d2 = T.d2;
+    const int b_raw = g * W + w;
+    // Inactive wavefronts (past the batch, or stopped) keep staging and
+    // reaching the barriers; they compute nothing and store nothing.
+    const int b = b_raw < T.B ? b_raw : T.B - 1;
+    bool skip = b_raw >= T.B;
+    const int st = T.state[b];
+    if (!STATS && !skip) {
+        if (st != 0) {
+            skip = true;
+        } else if (stop_before(T, b, k)) {
+            if (r == 0 && lane == 0) T.state[b] = k - 1;
+            skip = true;
+        }
+    }
+    if (!__syncthreads_or(!skip)) return;
+
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * d2 + (size_t)b * d2;
+    float *ab = T.a + (size_t)b * d1;
+    const float *mub = T.mu + (size_t)b * d1;
+    float bv[NCW], colpart[NCW];
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const int j = lane + 64 * c;
+        bv[c] = j < d2 ? bsrc[j] : 0.f;
+        colpart[c] = 0.f;
+    }
+    float rowerr = 0.f, losspart = 0.f;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    const int nchunk = (i1 - i0 + RS - 1) / RS;
+
+    float stage[NLD];
+    auto load_chunk = [&](int ch) {
+#pragma unroll
+        for (int u = 0; u < NLD; ++u) {
+            const int e = threadIdx.x + NT * u;
+            const int rr = e / D2P, j = e - rr * D2P;
+            const int i = i0 + ch * RS + rr;
+            stage[u] = (e < RS * D2P && j < d2 && i < i1) ? T.C[(size_t)i * d2 + j] : 0.f;
+        }
+    };
+    auto store_chunk = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < NLD; ++u) {
+            const int e = threadIdx.x + NT * u;
+            const int rr = e / D2P, j = e - rr * D2P;
+            if (e < RS * D2P) lds[buf * RS * D2P + e] = j < d2 ? -T.s * stage[u] : kPadCost;
+            (void)rr;
+        }
+    };
+    load_chunk(0);
+    store_chunk(0);
+    __syncthreads();
+    for (int ch = 0; ch < nchunk; ++ch) {
+        const int buf = ch & 1;
+        if (ch + 1 < nchunk) load_chunk(ch + 1);  // in flight while this chunk is computed
+        if (!skip) {
+            const int rows = min(RS, i1 - (i0 + ch * RS));
+            for (int rr = 0; rr < rows; ++rr) {
+                const int i = i0 + ch * RS + rr;
+                const LdsCost cost{lds + buf * RS * D2P + rr * D2P + lane};
+                row_step<NCW, STATS>(cost, ab[i], mub[i], ab + i, bv, colpart, rowerr, losspart, lane);
+            }
+        }
+        if (ch + 1 < nchunk) store_chunk(buf ^ 1);
+        __syncthreads();
+    }
+    if (skip) return;
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const int j = lane + 64 * c;
+        if (j < d2) T.part[pidx(T, 0, r, b, j)] = colpart[c];
+    }
+    const float lw = STATS ? wave_sum(losspart) : 0.f;
+    if (lane == 0) {
+        const int plane = STATS ? 2 : (k & 1);
+        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = rowerr;
+        if (STATS) T.lossp[(size_t)r * T.B + b] = lw;
     }
 }
 
@@ -328,14 +543,37 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
     }
 }
 
-// Row blocks: enough work-groups to fill the chip (>= ~2048 wavefronts), rows
-// per block a multiple of the wavefronts per group.
-void row_blocks(int B, int d1, int *R, int *RBS) {
-    int want = (2048 / kWaves + B - 1) / (B > 0 ? B : 1);
-    int maxR = (d1 + kWaves - 1) / kWaves;
-    int r = want < 1 ? 1 : (want > maxR ? maxR : want);
+// Which sweep serves a problem: the shared-cost sweep with W problems per
+// work-group when C is shared and the batch fills at least four wavefronts,
+// otherwise one problem per work-group.
+int shared_width(int B, int c_batched) {
+    if (c_batched) return 0;
+    if (B >= 8) return 8;
+    if (B >= 4) return 4;
+    return 0;
+}
+
+// Row blocks.  One problem per work-group: enough work-groups for ~2048
+// wavefronts, rows per block a multiple of the wavefronts per group.  Shared
+// cost: ~256 (wide rows) or ~512 work-groups, the count of row blocks a
+// multiple of 8 when the rows allow it so that a row block stays on one XCD.
+void row_blocks(int B, int d1, int d2, int c_batched, int *R, int *RBS) {
+    const int W = shared_width(B, c_batched);
+    int want, unit;
+    if (W) {
+        const int G = (B + W - 1) / W;
+        const int target = d2 > 1024 ? 256 : 512;
+        want = (target + G - 1) / G;
+        want = (want + 7) / 8 * 8;
+        unit = 1;
+    } else {
+        want = (2048 / kWaves + B - 1) / (B > 0 ? B : 1);
+        unit = kWaves;
+    }
+    const int maxR = (d1 + unit - 1) / unit;
+    const int r = want < 1 ? 1 : (want > maxR ? maxR : want);
     int rbs = (d1 + r - 1) / r;
-    rbs = (rbs + kWaves - 1) / kWaves * kWaves;
+    rbs = (rbs + unit - 1) / unit * unit;
     *RBS = rbs;
     *R = (d1 + rbs - 1) / rbs;
 }
@@ -346,10 +584,10 @@ struct Layout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-Layout layout(int B, int d1, int d2, int *R_out, int *RBS_out, int *JC_out) {
+Layout layout(int B, int d1, int d2, int c_batched, int *R_out, int *RBS_out, int *JC_out) {
     int R, RBS;
-    row_blocks(B, d1, &R, &RBS);
-    const int JC = (d2 + kThreads - 1) / kThreads;
+    row_blocks(B, d1, d2, c_batched, &R, &RBS);
+    const int JC = (d2 + kMergeThreads - 1) / kMergeThreads;
     Layout L;
     size_t off = 0;
     L.bbuf = off;
@@ -371,22 +609,52 @@ Layout layout(int B, int d1, int d2, int *R_out, int *RBS_out, int *JC_out) {
     return L;
 }
 
-template <int NCW, bool BATCHED>
-hipError_t run(const TiledArgs &T, hipStream_t st) {
-    const size_t lds = sizeof(float) * kWaves * NCW * 64;
+// Launch sequence: init, exact first v-update (+ merge), n sweeps with a merge
+// after each but the last, stats sweep, final.
+template <class Sweep, class Stats>
+hipError_t run_sequence(const TiledArgs &T, hipStream_t st, Sweep sweep, Stats stats) {
     const dim3 blk(kThreads);
     hipLaunchKernelGGL(sk_tiled_init, dim3(512), blk, 0, st, T);
     if (T.n_iter > 0) {
-        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), blk, 0, st, T);
-        hipLaunchKernelGGL(sk_tiled_merge<true>, dim3(T.JC, T.B), blk, 0, st, T, 0);
+        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+        const dim3 mblk(kMergeThreads);
+        hipLaunchKernelGGL(sk_tiled_merge<true>, dim3(T.JC, T.B), mblk, 0, st, T, 0);
         for (int k = 1; k <= T.n_iter; ++k) {
-            hipLaunchKernelGGL((sk_tiled_sweep<NCW, false, BATCHED>), dim3(T.R, T.B), blk, lds, st, T, k);
-            if (k < T.n_iter) hipLaunchKernelGGL(sk_tiled_merge<false>, dim3(T.JC, T.B), blk, 0, st, T, k);
+            sweep(k);
+            if (k < T.n_iter) hipLaunchKernelGGL(sk_tiled_merge<false>, dim3(T.JC, T.B), mblk, 0, st, T, k);
         }
     }
-    hipLaunchKernelGGL((sk_tiled_sweep<NCW, true, BATCHED>), dim3(T.R, T.B), blk, lds, st, T, 0);
+    stats();
     hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), blk, 0, st, T);
     return hipGetLastError();
+}
+
+template <int NCW, bool BATCHED>
+hipError_t run(const TiledArgs &T, hipStream_t st) {
+    const size_t lds = sizeof(float) * kWaves * NCW * 64;
+    const dim3 grid(T.R, T.B), blk(kThreads);
+    return run_sequence(
+        T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep<NCW, false, BATCHED>), grid, blk, lds, st, T, k); },
+        [&]() { hipLaunchKernelGGL((sk_tiled_sweep<NCW, true, BATCHED>), grid, blk, lds, st, T, 0); });
+}
+
+template <int NC4>
+hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
+    const size_t lds = sizeof(float) * kWaves * 4 * NC4 * 64;
+    const dim3 grid(T.R, T.B), blk(kThreads);
+    return run_sequence(
+        T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, false>), grid, blk, lds, st, T, k); },
+        [&]() { hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, true>), grid, blk, lds, st, T, 0); });
+}
+
+template <int NCW, int W>
+hipError_t run_shared(const TiledArgs &T, hipStream_t st) {
+    constexpr int RS = (64 / NCW) < 8 ? (64 / NCW) : 8;
+    const size_t lds = sizeof(float) * 2 * RS * NCW * 64;
+    const dim3 grid(T.R, (T.B + W - 1) / W), blk(64 * W);
+    return run_sequence(
+        T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, false>), grid, blk, lds, st, T, k); },
+        [&]() { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, true>), grid, blk, lds, st, T, 0); });
 }
 
 template <bool BATCHED>
@@ -399,22 +667,32 @@ hipError_t dispatch(const TiledArgs &T, int ncw, hipStream_t st) {
     return run<64, BATCHED>(T, st);
 }
 
-}  // namespace
-
-size_t tiled_workspace_bytes(int B, int d1, int d2, int /*c_batched*/) {
-    return layout(B, d1, d2, nullptr, nullptr, nullptr).total;
+template <int W>
+hipError_t dispatch_shared(const TiledArgs &T, int ncw, hipStream_t st) {
+    if (ncw <= 4) return run_shared<4, W>(T, st);
+    if (ncw <= 8) return run_shared<8, W>(T, st);
+    if (ncw <= 13) return run_shared<13, W>(T, st);
+    if (ncw <= 16) return run_shared<16, W>(T, st);
+    if (ncw <= 32) return run_shared<32, W>(T, st);
+    return run_shared<64, W>(T, st);
 }
 
-bool tiled_fits(int B, int d1, int d2) {
+}  // namespace
+
+size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched) {
+    return layout(B, d1, d2, c_batched, nullptr, nullptr, nullptr).total;
+}
+
+bool tiled_fits(int B, int d1, int d2, int c_batched) {
     int R, RBS;
-    row_blocks(B, d1, &R, &RBS);
+    row_blocks(B, d1, d2, c_batched, &R, &RBS);
     return d2 <= kTiledMaxD2 && B <= 65535 && R <= 65535;
 }
 
 hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     TiledArgs T;
     int R, RBS, JC;
-    const Layout L = layout(a.B, a.d1, a.d2, &R, &RBS, &JC);
+    const Layout L = layout(a.B, a.d1, a.d2, a.c_batched, &R, &RBS, &JC);
     char *base = static_cast<char *>(ws);
     T.mu = a.mu;
     T.nu = a.nu;
@@ -442,6 +720,17 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     T.s = a.s;
     T.tol = a.tol;
     const int ncw = (a.d2 + 63) / 64;
+    const int W = shared_width(a.B, a.c_batched);
+    if (W == 8) return dispatch_shared<8>(T, ncw, st);
+    if (W == 4) return dispatch_shared<4>(T, ncw, st);
+    if (a.c_batched && a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0) {
+        const int nc4 = (a.d2 + 255) / 256;
+        if (nc4 <= 1) return run_stream<1>(T, st);
+        if (nc4 <= 2) return run_stream<2>(T, st);
+        if (nc4 <= 4) return run_stream<4>(T, st);
+        if (nc4 <= 8) return run_stream<8>(T, st);
+        return run_stream<16>(T, st);
+    }
     if (a.c_batched) return dispatch<true>(T, ncw, st);
     return dispatch<false>(T, ncw, st);
 }

@@ -306,3 +306,24 @@ def test_tiled_deterministic_bitwise():
     b = _gpu(prob)
     for k in a:
         np.testing.assert_array_equal(a[k], b[k])
+
+
+@pytest.mark.parametrize("B,d1,d2,c_batched", [
+    (5, 200, 300, False),    # shared cost, 4 problems per work-group (+1 idle-padded group)
+    (9, 150, 260, False),    # shared cost, 8 problems per work-group, 7 idle wavefronts in the last group
+    (3, 160, 301, True),     # per-sample cost, d2 % 4 != 0: scalar per-problem sweep
+    (3, 129, 516, True),     # per-sample cost, 128-bit streaming sweep with a ragged last vector
+    (2, 300, 200, False),    # shared cost, batch too small for the shared sweep
+])
+def test_tiled_kernel_variants(B, d1, d2, c_batched):
+    prob = workloads.random_problem(seed=B * 1000 + d2, B=B, d1=d1, d2=d2, lam=0.08, n_iter=35,
+                                    c_batched=c_batched, zero_frac=0.1)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_tiled_variants_early_stop_shared():
+    """Early stop inside the shared-cost sweep (stopped problems keep staging)."""
+    prob = workloads.random_problem(seed=31, B=10, d1=180, d2=200, lam=0.1, n_iter=300, tol=2e-4)
+    gpu, ref = check_forward(prob)
+    assert np.all(gpu["iters"] < 300)
