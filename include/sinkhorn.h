@@ -1,11 +1,12 @@
 /*
- * sinkhorn.h -- C ABI of the MI355X (gfx950) batched log-domain Sinkhorn library.
+ * sinkhorn.h -- C ABI of the MI355X (gfx950) batched Sinkhorn library.
  *
  * Method: Viehmann, "Implementation of batched Sinkhorn iterations for
  * entropy-regularized Wasserstein loss" (arXiv:1907.01729).  For a batch of
  * histogram pairs (mu_b, nu_b) and a cost C (shared, or one per sample) the
- * library runs the log-domain Sinkhorn iteration (Section 3, eq. (log_sk), with
- * the sign of the batched form in Section 4), returns the log-scalings, the
+ * library runs the Sinkhorn iteration in the log domain (Section 3, eq. (log_sk),
+ * with the sign of the batched form in Section 4) or, where fp32 range allows,
+ * the same iterates in the plain form (eq. (sk_plain)), returns the log-scalings, the
  * loss E^0 (Section 5) and the marginal error, and computes the
  * Lagrange-multiplier gradient (Section 2).
  *
@@ -83,6 +84,17 @@ SK_API size_t sinkhorn_workspace_bytes(const sk_problem *p);
  * from alpha^0 = 0 on the support of mu (-inf off it).  With n_iter = 0,
  * alpha = beta = 0 on the supports.
  *
+ * For max(d1, d2) <= 128 the same iterates are first computed in the plain
+ * form of eq. (sk_plain), u = mu / (K v), v = nu / (K^T u), with K scaled by
+ * its largest entry (on the matrix cores when C is shared); a problem whose
+ * scaled cost spans more than 64 bits, or whose sums or scalings leave a
+ * guarded fp32 range at any iteration, is re-solved from the start by the
+ * log-domain kernel launched right after it on the same stream.  Diagnostic
+ * switch (environment variable SK_RESIDENT_FORM, read at every call): "log"
+ * runs the log-domain kernel only; "plain" runs the plain form only, leaving
+ * the problems it cannot keep in range with iters = -1 and their other
+ * outputs unspecified.
+ *
  *   mu        [B, d1]              input histograms
  *   nu        [B, d2]
  *   C         [d1, d2] or [B, d1, d2] (see c_batched)
@@ -127,8 +139,8 @@ SK_API const char *sinkhorn_status_string(sk_status s);
 
 /*
  * Which kernel family sinkhorn_forward uses for *p:
- *   1 = resident (one wavefront per problem; C and potentials on-chip for the
- *       whole iteration; max(d1, d2) <= 128),
+ *   1 = resident (max(d1, d2) <= 128: C and potentials on-chip for the whole
+ *       iteration; plain form with the log-domain fallback described above),
  *   2 = tiled sweep (one pass over C per iteration, column partials merged
  *       across row blocks).
  * Returns 0 for an invalid problem.

@@ -2,6 +2,8 @@
 // regime dispatch and launches.  No allocation, no synchronisation.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include "sk_internal.h"
 
@@ -19,6 +21,20 @@ sk_status check_problem(const sk_problem *p) {
     if (!(p->lambda > 0.f) || !isfinite(p->lambda)) return SK_ERR_LAMBDA;
     if (p->n_iter < 0 || !isfinite(p->tol)) return SK_ERR_ITERS;
     return SK_OK;
+}
+
+// Which resident kernel runs (diagnostic switch, environment variable
+// SK_RESIDENT_FORM): "log" forces the log-domain kernel, "plain" runs the
+// plain-form kernel alone (problems it cannot take stay at iters = -1),
+// anything else the plain form with the log-domain kernel as its fallback.
+constexpr int kFormAuto = 0, kFormLog = 1, kFormPlain = 2;
+
+int resident_form() {
+    const char *e = getenv("SK_RESIDENT_FORM");
+    if (!e) return kFormAuto;
+    if (!strcmp(e, "log")) return kFormLog;
+    if (!strcmp(e, "plain")) return kFormPlain;
+    return kFormAuto;
 }
 
 }  // namespace
@@ -78,8 +94,23 @@ sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu
     a.tol = p->tol;
     a.s = sk::kLog2eHost / p->lambda;
 
+    a.only_flagged = 0;
+
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = sk::resident_fits(p->d1, p->d2) ? sk::launch_resident(a, s) : sk::launch_tiled(a, workspace, s);
+    hipError_t e;
+    if (!sk::resident_fits(p->d1, p->d2)) {
+        e = sk::launch_tiled(a, workspace, s);
+    } else {
+        const int form = resident_form();
+        if (form != kFormLog && (sk::launch_resident_mfma(a, s, &e) || sk::launch_resident_plain(a, s, &e))) {
+            if (e == hipSuccess && form == kFormAuto) {
+                a.only_flagged = 1;
+                e = sk::launch_resident(a, s);
+            }
+        } else {
+            e = sk::launch_resident(a, s);
+        }
+    }
     return e == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 

@@ -18,6 +18,9 @@ struct FwdArgs {
     int B, d1, d2, n_iter, c_batched;
     float lambda, tol;
     float s;  // log2(e) / lambda
+    // Set when a plain-form launch ran first: solve only the problems it
+    // marked with iters = -1 and leave the others untouched.
+    int only_flagged;
 };
 
 struct BwdArgs {
@@ -33,6 +36,12 @@ constexpr int kResidentMaxD = 128;
 
 bool resident_fits(int d1, int d2);
 hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
+// Plain-form resident kernel: returns false (and launches nothing) when it
+// does not take the shape; otherwise *err is the launch status.  Problems it
+// cannot keep in range come back with iters = -1.
+bool launch_resident_plain(const FwdArgs &a, hipStream_t st, hipError_t *err);
+// Same contract; a cost shared by the batch only, products on the matrix cores.
+bool launch_resident_mfma(const FwdArgs &a, hipStream_t st, hipError_t *err);
 
 // The tiled sweep keeps a whole cost row in one wavefront's registers.
 constexpr int kTiledMaxD2 = 4096;

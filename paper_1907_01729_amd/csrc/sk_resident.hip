@@ -221,6 +221,16 @@ __global__ __launch_bounds__(64 * WPB) void sk_resident_kernel(FwdArgs A) {
     const int b = blockIdx.x * WPB + w;
     const int d1 = A.d1, d2 = A.d2;
 
+    if (A.only_flagged) {
+        // Skip the work-group unless one of its problems was left to this kernel.
+        bool any = false;
+#pragma unroll
+        for (int v = 0; v < WPB; ++v) {
+            const int bb = blockIdx.x * WPB + v;
+            any |= bb < A.B && A.iters[bb] == -1;
+        }
+        if (!any) return;
+    }
     // Stage cl in the lane-blocked layout; cells outside the problem hold kPadCost.
     if (!BATCHED) {
         for (int idx = threadIdx.x; idx < N * N * 64; idx += 64 * WPB) {
@@ -240,6 +250,7 @@ __global__ __launch_bounds__(64 * WPB) void sk_resident_kernel(FwdArgs A) {
     }
     __syncthreads();
     if (b >= A.B) return;
+    if (A.only_flagged && A.iters[b] != -1) return;
 
     const Tile<N> cl{lds + (BATCHED ? w * N * N * 64 : 0) + lane};
     const float *mub = A.mu + (size_t)b * d1;

@@ -92,21 +92,29 @@ def check_backward(prob, gpu, ref, idx=None, grad_C=False, seed=0):
         assert e3 <= GRAD_RTOL
 
 
+@pytest.fixture(params=["auto", "log"])
+def form(request, monkeypatch):
+    """Resident regime: the plain-form kernel with its log-domain fallback
+    (the default), or the log-domain kernel alone."""
+    monkeypatch.setenv("SK_RESIDENT_FORM", request.param)
+    return request.param
+
+
 # ---------------------------------------------------------------- workloads
 
-def test_tiny_full():
+def test_tiny_full(form):
     prob = workloads.make_config(1)
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_label_subset_full_iterations():
+def test_label_subset_full_iterations(form):
     prob = workloads.make_config(2, B=48)
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_label_full_batch_sampled():
+def test_label_full_batch_sampled(form):
     """The benchmark's launch: B=1024, d=100, 200 iterations; the oracle checks
     a sample of the problems (each problem is independent)."""
     prob = workloads.make_config(2)
@@ -121,13 +129,13 @@ def test_label_full_batch_sampled():
 
 @pytest.mark.parametrize("d1,d2", [(16, 16), (17, 9), (32, 31), (33, 64), (65, 100), (104, 37), (105, 128),
                                    (128, 128), (1, 7), (7, 1), (1, 1)])
-def test_shapes_every_template(d1, d2):
+def test_shapes_every_template(d1, d2, form):
     prob = workloads.random_problem(seed=d1 * 1000 + d2, B=5, d1=d1, d2=d2, lam=0.1, n_iter=40)
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_zero_masses():
+def test_zero_masses(form):
     prob = workloads.random_problem(seed=7, B=6, d1=37, d2=100, lam=0.1, n_iter=60, zero_frac=0.25)
     assert (prob.mu == 0).any() and (prob.nu == 0).any()
     gpu, ref = check_forward(prob)
@@ -139,39 +147,39 @@ def test_zero_masses():
     assert np.all(out["grad_mu"].cpu().numpy()[prob.mu == 0] == 0)
 
 
-def test_per_sample_cost_resident():
+def test_per_sample_cost_resident(form):
     prob = workloads.random_problem(seed=8, B=5, d1=20, d2=30, lam=0.05, n_iter=80, c_batched=True)
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
 @pytest.mark.parametrize("n_iter", [0, 1, 2])
-def test_few_iterations(n_iter):
+def test_few_iterations(n_iter, form):
     prob = workloads.random_problem(seed=9, B=3, d1=12, d2=9, lam=0.2, n_iter=n_iter)
     gpu, ref = check_forward(prob, merr_rtol=1e-3)
     assert np.all(gpu["iters"] == n_iter)
 
 
-def test_single_sample_batch():
+def test_single_sample_batch(form):
     prob = workloads.random_problem(seed=10, B=1, d1=50, d2=70, lam=0.05, n_iter=100)
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_early_stop_per_sample():
+def test_early_stop_per_sample(form):
     prob = workloads.random_problem(seed=11, B=6, d1=30, d2=40, lam=0.1, n_iter=400, tol=1e-4)
     gpu, ref = check_forward(prob)
     assert np.all(gpu["iters"] < 400) and len(set(gpu["iters"].tolist())) > 1
     assert np.all(gpu["marg_err"] <= 1.5e-4)
 
 
-def test_unreachable_tol_runs_all_iterations():
+def test_unreachable_tol_runs_all_iterations(form):
     prob = workloads.random_problem(seed=12, B=3, d1=20, d2=20, lam=0.01, n_iter=30, tol=1e-9)
     gpu, ref = check_forward(prob)
     assert np.all(gpu["iters"] == 30)
 
 
-def test_large_lambda_independent_coupling():
+def test_large_lambda_independent_coupling(form):
     prob = workloads.random_problem(seed=13, B=4, d1=20, d2=25, lam=1e3, n_iter=5)
     gpu, ref = check_forward(prob)
     indep = np.einsum("bi,ij,bj->b", prob.mu.astype(np.float64), prob.C[0].astype(np.float64),
@@ -179,7 +187,7 @@ def test_large_lambda_independent_coupling():
     assert np.allclose(gpu["loss"], indep, rtol=1e-3)
 
 
-def test_small_lambda_1d_grid_w1():
+def test_small_lambda_1d_grid_w1(form):
     """lambda = 1e-3 on a 1-D grid (C/lambda up to 1000): exercises the exact
     logsumexp fallbacks; E^0 approaches the closed-form W1."""
     prob = workloads.random_problem(seed=14, B=4, d1=100, d2=100, lam=1e-3, n_iter=300, cost="grid1d")
@@ -190,7 +198,7 @@ def test_small_lambda_1d_grid_w1():
         assert gpu["loss"][k] == pytest.approx(w1, abs=1e-2 + 5 * gpu["marg_err"][k])
 
 
-def test_deterministic_bitwise():
+def test_deterministic_bitwise(form):
     prob = workloads.make_config(2, B=64)
     a = _gpu(prob)
     b = _gpu(prob)
@@ -198,7 +206,7 @@ def test_deterministic_bitwise():
         np.testing.assert_array_equal(a[k], b[k])
 
 
-def test_autograd_wrapper():
+def test_autograd_wrapper(form):
     prob = workloads.random_problem(seed=15, B=4, d1=24, d2=24, lam=0.1, n_iter=50)
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
     mu = t(prob.mu).requires_grad_()
@@ -214,6 +222,49 @@ def test_autograd_wrapper():
 
 
 # ---------------------------------------------------------------- tiled regime (max(d1, d2) > 128)
+
+# ---------------------------------------------------------------- plain form and its fallback
+
+def test_plain_form_takes_in_range_problems(monkeypatch):
+    """The plain-form kernel alone (no fallback launch) solves every label
+    problem (cost spread 54 bits) and leaves a lambda = 1e-3 grid problem
+    (spread > 1000 bits) to the log-domain kernel: iters = -1."""
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    prob = workloads.make_config(2, B=32)
+    gpu, ref = check_forward(prob)
+    assert np.all(gpu["iters"] == prob.n_iter)
+    check_backward(prob, gpu, ref, grad_C=True)
+    far = workloads.random_problem(seed=16, B=3, d1=40, d2=40, lam=1e-3, n_iter=20, cost="grid1d")
+    assert np.all(_gpu(far)["iters"] == -1)
+
+
+def test_plain_fallback_mixed_batch(monkeypatch):
+    """Per-sample costs where every third problem's cost spread exceeds the
+    plain form's range: with the fallback every problem matches the oracle;
+    without it exactly those problems come back unsolved."""
+    prob = workloads.random_problem(seed=17, B=9, d1=50, d2=60, lam=0.05, n_iter=80, c_batched=True)
+    far = np.arange(prob.B) % 3 == 0
+    prob.C[far] *= 3.0  # spread 3 * 28.9 bits > 64
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    alone = _gpu(prob)
+    assert np.all((alone["iters"] == -1) == far)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+    near = ~far
+    for k in ("alpha", "beta", "loss", "marg_err", "iters"):
+        np.testing.assert_array_equal(gpu[k][near], alone[k][near])
+
+
+def test_plain_early_stop_agrees_with_log(monkeypatch):
+    prob = workloads.random_problem(seed=18, B=8, d1=64, d2=48, lam=0.1, n_iter=300, tol=1e-5)
+    out = {}
+    for f in ("plain", "log"):
+        monkeypatch.setenv("SK_RESIDENT_FORM", f)
+        out[f] = check_forward(prob)[0]
+    assert np.all(out["plain"]["iters"] >= 0)
+    assert np.all(np.abs(out["plain"]["iters"] - out["log"]["iters"]) <= 1)
+
 
 def test_image_reduced_batch():
     prob = workloads.make_config(3, B=4, n_iter=60)
