@@ -41,8 +41,8 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the onl
 struct TiledArgs {
     const float *mu, *nu, *C;
     float *a;        // [B, d1] base-2 potentials (the alpha output buffer)
-    float *bbuf;     // [2][B, d2] base-2 column potentials, ping-pong by iteration parity
-    float *part;     // [2][R][B, d2] column partials (plane 1 only for the exact pass)
+    float *bbuf;     // [2][B, d2p] base-2 column potentials, ping-pong by iteration parity
+    float *part;     // [2][R][B, d2p] column partials (plane 1 only for the exact pass)
     float *rowerr;   // [3][R][B] row-error partials: planes 0/1 by iteration parity, 2 for stats
     float *lossp;    // [R][B] loss partials (stats)
     float *colerr;   // [B][JC] column-error partials of the merge
@@ -50,11 +50,13 @@ struct TiledArgs {
     float *alpha_out, *beta_out, *loss_out, *merr_out;
     int32_t *iters_out;
     int B, d1, d2, R, RBS, JC, n_iter, c_batched;
+    int d2p;  // row stride of bbuf and part: d2 rounded up to the sweep's column width
+              // (entries past d2 stay 0), so sweeps load and store whole rows unmasked
     float s, tol;
 };
 
 __device__ __forceinline__ size_t pidx(const TiledArgs &T, int plane, int r, int b, int j) {
-    return (((size_t)plane * T.R + r) * T.B + b) * (size_t)T.d2 + j;
+    return (((size_t)plane * T.R + r) * T.B + b) * (size_t)T.d2p + j;
 }
 
 // Work-group sum in a fixed order (deterministic); `red` holds kWaves floats.
@@ -73,9 +75,15 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
     const size_t n = (size_t)T.B * T.d1;
     for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < n; u += (size_t)gridDim.x * kThreads)
         T.a[u] = T.mu[u] > 0.f ? 0.f : neg_inf();
-    const size_t m = (size_t)T.B * T.d2;
-    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < m; u += (size_t)gridDim.x * kThreads)
-        T.bbuf[u] = T.nu[u] > 0.f ? 0.f : neg_inf();  // b^0 (only used when n_iter == 0)
+    // Both planes: b^0 in plane 0 (only read when n_iter == 0), zeros past d2.
+    const size_t m = (size_t)2 * T.B * T.d2p;
+    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < m; u += (size_t)gridDim.x * kThreads) {
+        const size_t row = u / T.d2p;
+        const int j = (int)(u - row * T.d2p);
+        float v = 0.f;
+        if (row < (size_t)T.B && j < T.d2 && !(T.nu[row * T.d2 + j] > 0.f)) v = neg_inf();
+        T.bbuf[u] = v;
+    }
     for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < (size_t)T.B; u += (size_t)gridDim.x * kThreads)
         T.state[u] = 0;
 }
@@ -134,19 +142,19 @@ __global__ __launch_bounds__(kMergeThreads) void sk_tiled_merge(TiledArgs T, int
             float S = 0.f;
             for (int r = 0; r < T.R; ++r) S += T.part[pidx(T, 1, r, b, j)] * ex2(T.part[pidx(T, 0, r, b, j)] - M);
             if (nuj > 0.f) bnew = log2f(nuj) - (M + lg2(S));
-            T.bbuf[(size_t)1 * T.B * T.d2 + (size_t)b * T.d2 + j] = bnew;
+            T.bbuf[(size_t)1 * T.B * T.d2p + (size_t)b * T.d2p + j] = bnew;
         } else {
             float cs = 0.f;
             for (int r = 0; r < T.R; ++r) cs += T.part[pidx(T, 0, r, b, j)];
             err = fabsf(cs - nuj);
             if (nuj > 0.f) {
-                const float bold = T.bbuf[(size_t)(k & 1) * T.B * T.d2 + (size_t)b * T.d2 + j];
+                const float bold = T.bbuf[(size_t)(k & 1) * T.B * T.d2p + (size_t)b * T.d2p + j];
                 if (cs >= kSumLo && cs <= kSumHi)
                     bnew = bold + log2f(nuj) - lg2(cs);
                 else
                     bnew = log2f(nuj) - col_lse_exact(T, b, j);
             }
-            T.bbuf[(size_t)((k + 1) & 1) * T.B * T.d2 + (size_t)b * T.d2 + j] = bnew;
+            T.bbuf[(size_t)((k + 1) & 1) * T.B * T.d2p + (size_t)b * T.d2p + j] = bnew;
         }
     }
     if (!EXACT) {
@@ -262,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
         }
     }
     const int K = STATS ? (st ? st : T.n_iter) : k;
-    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * d2 + (size_t)b * d2;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
     const float *Cb = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0);
     float *ab = T.a + (size_t)b * d1;
     const float *mub = T.mu + (size_t)b * d1;
@@ -271,7 +279,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
 #pragma unroll
     for (int c = 0; c < NCW; ++c) {
         const int j = lane + 64 * c;
-        bv[c] = j < d2 ? bsrc[j] : 0.f;
+        bv[c] = bsrc[j];  // 0 past d2 (padded stride)
         colpart[c] = 0.f;
     }
     float rowerr = 0.f, losspart = 0.f;
@@ -347,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_stream(TiledArgs T, i
         }
     }
     const int K = STATS ? (st ? st : T.n_iter) : k;
-    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * d2 + (size_t)b * d2;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
     const float *Cb = T.C + (size_t)b * d1 * d2;
     float *ab = T.a + (size_t)b * d1;
     const float *mub = T.mu + (size_t)b * d1;
@@ -356,7 +364,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_stream(TiledArgs T, i
 #pragma unroll
     for (int cc = 0; cc < NCW; ++cc) {
         const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
-        bv[cc] = j < d2 ? bsrc[j] : 0.f;
+        bv[cc] = bsrc[j];  // 0 past d2 (padded stride)
         colpart[cc] = 0.f;
     }
     auto load_row = [&](float (&dst)[NCW], int i) {
@@ -415,19 +423,76 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_stream(TiledArgs T, i
     }
 }
 
-// Sweep for a cost shared by the batch (Section 4's setting): a work-group of
-// W wavefronts = W problems of group g walks the rows of row block r; chunks
-// of RS cost rows are staged once in LDS (scaled, padded, double-buffered) and
-// read by all W wavefronts, so each cost element leaves L2 once per W
+// Sweep for a cost shared by the batch (Section 4's setting).
+//
+// A work-group of W wavefronts = W problems of group g walks the rows of row
+// block r.  Chunks of RS raw cost rows are copied into LDS by direct
+// global->LDS loads (no registers, no VALU work), double-buffered: the next
+// chunk is in flight while the current one is computed, and every staged
+// element is read by all W wavefronts, so the cost leaves L2 once per W
 // problems.  Work-groups of the same row block share an XCD (block index
-// r + R g with R a multiple of 8), so the row block leaves HBM once.
-template <int NCW, int W, bool STATS>
+// r + R g with R a multiple of 8), so a row block leaves HBM once.
+//
+// Per cell: one add (a_i + b_j), one fma (- s C_ij), one exp, one add (row
+// sum) and one fma (column sum).  RB rows are reduced together: their row
+// sums share one transposed wavefront all-reduce (permlane swaps pack the RB
+// partial vectors into one register before the 16-lane DPP stages).  The row
+// potentials a_i and log2 mu_i of 64 rows sit in one register each (lane =
+// row), are read with readlane and prefetched a segment ahead; the updated
+// a_i are collected the same way and stored once per 64 rows.
+constexpr float kPadC = 1.0e30f;  // raw cost of padding cells: exp underflows to 0, 0 * cl stays finite
+constexpr int kSegs = 4;          // row blocks of the shared-cost sweep hold at most 64 kSegs rows
+
+// All-reduce of RB per-lane partials (RB = 1, 2 or 4); every lane gets the
+// same bits.  Packing: a permlane32 swap pairs (p0, p1) so that lanes < 32
+// carry p0's half-sums and lanes >= 32 p1's; a permlane16 swap then packs
+// four vectors into the four 16-lane rows (p0, p2, p1, p3).
+__device__ __forceinline__ LanePair swap32x(float x, float y) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ LanePair swap16x(float x, float y) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ float sum16(float v) {  // all-reduce within each 16-lane row
+    v = sum_q(v);
+    return v + dpp<kRowRor8>(v);
+}
+__device__ __forceinline__ float uni(float v, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+template <int RB>
+__device__ __forceinline__ void allreduce_rows(const float (&p)[RB], float (&s)[RB]) {
+    if constexpr (RB == 1) {
+        s[0] = uni(wave_sum(p[0]), 0);
+    } else if constexpr (RB == 2) {
+        const LanePair a = swap32x(p[0], p[1]);
+        float v = a.lo + a.hi;
+        const LanePair b = swap16(v);
+        v = sum16(b.lo + b.hi);
+        s[0] = uni(v, 0);
+        s[1] = uni(v, 32);
+    } else {
+        static_assert(RB == 4, "RB must be 1, 2 or 4");
+        const LanePair a = swap32x(p[0], p[1]);
+        const LanePair b = swap32x(p[2], p[3]);
+        const LanePair c = swap16x(a.lo + a.hi, b.lo + b.hi);
+        const float v = sum16(c.lo + c.hi);
+        s[0] = uni(v, 0);
+        s[2] = uni(v, 16);
+        s[1] = uni(v, 32);
+        s[3] = uni(v, 48);
+    }
+}
+
+template <int NCW, int W, int RS, int RB, bool VEC4, bool STATS>
 __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int k) {
-    constexpr int D2P = NCW * 64;              // padded row length in LDS
-    constexpr int RS = (64 / NCW) < 8 ? (64 / NCW) : 8;  // rows per staged chunk (2 x RS x D2P <= 32 KB)
+    constexpr int D2P = NCW * 64;  // LDS row length (columns beyond d2 hold kPadC)
     constexpr int NT = 64 * W;
-    constexpr int NLD = (RS * D2P + NT - 1) / NT;  // staging loads per thread
-    extern __shared__ float lds[];                 // [2][RS][D2P]
+    constexpr int VW = VEC4 ? 4 : 1;  // floats per lane per global->LDS load
+    static_assert(RS % RB == 0 && 64 % RS == 0, "chunks must tile 64-row segments");
+    extern __shared__ float lds[];  // [2][RS][D2P]
     const int r = blockIdx.x, g = blockIdx.y;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int d1 = T.d1, d2 = T.d2;
@@ -447,62 +512,167 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     }
     if (!__syncthreads_or(!skip)) return;
 
+    // Every LDS word starts finite (padding cost), so rows past the block and
+    // columns past d2 give plan entries of exactly 0.
+    for (int u = threadIdx.x; u < 2 * RS * D2P; u += NT) lds[u] = kPadC;
+    __syncthreads();
+
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    const int nrows = i1 - i0;
+    const int nchunk = (nrows + RS - 1) / RS;
+    const int lpr = (d2 + 64 * VW - 1) / (64 * VW);  // wavefront loads per cost row
+    auto issue_chunk = [&](int ch) {
+        float *base = lds + (ch & 1) * RS * D2P;
+        for (int q = w; q < RS * lpr; q += W) {  // wavefront-uniform
+            const int rr = q / lpr, sg = q - rr * lpr;
+            const int i = i0 + ch * RS + rr;
+            const int u = sg * 64 + lane;
+            if (i < i1 && u * VW < d2) {
+                const float *src = T.C + (size_t)i * d2 + (size_t)u * VW;
+                auto *dst = (__attribute__((address_space(3))) void *)(base + rr * D2P + sg * 64 * VW);
+                if constexpr (VEC4)
+                    __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+                else
+                    __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
+            }
+        }
+    };
+    issue_chunk(0);
+
     const int K = STATS ? (st ? st : T.n_iter) : k;
-    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * d2 + (size_t)b * d2;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
     float *ab = T.a + (size_t)b * d1;
     const float *mub = T.mu + (size_t)b * d1;
+    const float ns = -T.s;
     float bv[NCW], colpart[NCW];
 #pragma unroll
     for (int c = 0; c < NCW; ++c) {
         const int j = lane + 64 * c;
-        bv[c] = j < d2 ? bsrc[j] : 0.f;
+        bv[c] = bsrc[j];  // 0 past d2 (padded stride)
         colpart[c] = 0.f;
     }
+    // Row state of the block, 64 rows per register (lane = row), loaded
+    // before the first barrier; row blocks of this sweep have <= 64 kSegs rows.
+    float a_s[kSegs], mu_s[kSegs];
+#pragma unroll
+    for (int q = 0; q < kSegs; ++q) {
+        const int i = i0 + 64 * q + lane;
+        a_s[q] = i < i1 ? ab[i] : neg_inf();
+        mu_s[q] = i < i1 ? mub[i] : 0.f;
+    }
+    float a_seg = 0.f, mu_seg = 0.f, lmu_seg = 0.f, a_out = 0.f;
     float rowerr = 0.f, losspart = 0.f;
-    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
-    const int nchunk = (i1 - i0 + RS - 1) / RS;
 
-    float stage[NLD];
-    auto load_chunk = [&](int ch) {
-#pragma unroll
-        for (int u = 0; u < NLD; ++u) {
-            const int e = threadIdx.x + NT * u;
-            const int rr = e / D2P, j = e - rr * D2P;
-            const int i = i0 + ch * RS + rr;
-            stage[u] = (e < RS * D2P && j < d2 && i < i1) ? T.C[(size_t)i * d2 + j] : 0.f;
-        }
-    };
-    auto store_chunk = [&](int buf) {
-#pragma unroll
-        for (int u = 0; u < NLD; ++u) {
-            const int e = threadIdx.x + NT * u;
-            const int rr = e / D2P, j = e - rr * D2P;
-            if (e < RS * D2P) lds[buf * RS * D2P + e] = j < d2 ? -T.s * stage[u] : kPadCost;
-            (void)rr;
-        }
-    };
-    load_chunk(0);
-    store_chunk(0);
-    __syncthreads();
     for (int ch = 0; ch < nchunk; ++ch) {
-        const int buf = ch & 1;
-        if (ch + 1 < nchunk) load_chunk(ch + 1);  // in flight while this chunk is computed
-        if (!skip) {
-            const int rows = min(RS, i1 - (i0 + ch * RS));
-            for (int rr = 0; rr < rows; ++rr) {
-                const int i = i0 + ch * RS + rr;
-                const LdsCost cost{lds + buf * RS * D2P + rr * D2P + lane};
-                row_step<NCW, STATS>(cost, ab[i], mub[i], ab + i, bv, colpart, rowerr, losspart, lane);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wavefront's loads of chunk ch have landed
+        __syncthreads();                     // ... and every other wavefront's
+        if (ch + 1 < nchunk) issue_chunk(ch + 1);
+        const float *cbuf = lds + (ch & 1) * RS * D2P + lane;
+#pragma unroll
+        for (int rb = 0; rb < RS; rb += RB) {
+            const int rel = ch * RS + rb;
+            if (rel >= nrows) break;
+            if ((rel & 63) == 0) {  // next 64-row segment
+                const int sg = rel >> 6;
+                a_seg = a_s[0];
+                mu_seg = mu_s[0];
+#pragma unroll
+                for (int q = 1; q < kSegs; ++q) {
+                    a_seg = sg == q ? a_s[q] : a_seg;
+                    mu_seg = sg == q ? mu_s[q] : mu_seg;
+                }
+                lmu_seg = mu_seg > 0.f ? lg2(mu_seg) : neg_inf();
+                a_out = a_seg;
+            }
+            if (!skip) {
+                const int rr0 = rel & 63;
+                float ai[RB], mui[RB], e[RB][NCW], p[RB], rs[RB], f[RB];
+#pragma unroll
+                for (int q = 0; q < RB; ++q) {
+                    ai[q] = uni(a_seg, rr0 + q);
+                    mui[q] = uni(mu_seg, rr0 + q);
+                    const float *crow = cbuf + (rb + q) * D2P;
+#pragma unroll
+                    for (int c = 0; c < NCW; ++c) {
+                        // Wide rows: at most 16 staged values in flight, so that the
+                        // plan entries, bv and colpart keep their registers.
+                        if (NCW > 32 && c % 16 == 0 && c > 0) __asm__ volatile("" ::: "memory");
+                        e[q][c] = ex2(__builtin_fmaf(crow[64 * c], ns, ai[q] + bv[c]));
+                    }
+                    p[q] = tree_sum<NCW>(e[q]);
+                }
+                allreduce_rows<RB>(p, rs);
+                bool exact[RB];
+#pragma unroll
+                for (int q = 0; q < RB; ++q) {
+                    exact[q] = false;
+                    if (STATS) {
+                        const float *crow = cbuf + (rb + q) * D2P;
+                        if (mui[q] > 0.f) rowerr += fabsf(rs[q] - mui[q]);
+                        __asm__ volatile("" ::: "memory");  // re-read the staged row
+#pragma unroll
+                        for (int c = 0; c < NCW; ++c) losspart = __builtin_fmaf(e[q][c], crow[64 * c] * ns, losspart);
+                        f[q] = 1.f;
+                    } else if (!(mui[q] > 0.f)) {  // zero mass (or past the block): a_i = -inf, plan row 0
+                        f[q] = 0.f;
+                    } else if (rs[q] >= kSumLo && rs[q] <= kSumHi) {
+                        const float an = ai[q] + uni(lmu_seg, rr0 + q) - lg2(rs[q]);
+                        f[q] = ex2(an - ai[q]);
+                        rowerr += fabsf(f[q] * rs[q] - mui[q]);
+                        a_out = lane == rr0 + q ? an : a_out;
+                    } else {
+                        f[q] = 0.f;  // this row is redone exactly below
+                        exact[q] = true;
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < RB; ++q)
+#pragma unroll
+                    for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[q][c], f[q], colpart[c]);
+                if (!STATS) {
+#pragma unroll
+                    for (int q = 0; q < RB; ++q) {
+                        if (!exact[q]) continue;
+                        // The shifted row sum left [2^-64, 2^64]: exact u-update
+                        // of this row (max, then sum) from the staged cost, and
+                        // its plan entries rebuilt from the new potential.
+                        const float *crow = cbuf + (rb + q) * D2P;
+                        float m = neg_inf();
+#pragma unroll
+                        for (int c = 0; c < NCW; ++c) m = fmaxf(m, __builtin_fmaf(crow[64 * c], ns, bv[c]));
+                        m = wave_max(m);
+                        // Re-read the staged row in each pass rather than keep
+                        // it in registers (it would not fit beside bv and colpart).
+                        __asm__ volatile("" ::: "memory");
+                        float s2 = 0.f;
+#pragma unroll
+                        for (int c = 0; c < NCW; ++c) s2 += ex2(__builtin_fmaf(crow[64 * c], ns, bv[c]) - m);
+                        s2 = wave_sum(s2);
+                        const float an = uni(lmu_seg, rr0 + q) - (m + lg2(s2));
+                        __asm__ volatile("" ::: "memory");
+                        float rsum = 0.f;
+#pragma unroll
+                        for (int c = 0; c < NCW; ++c) {
+                            const float v = ex2(__builtin_fmaf(crow[64 * c], ns, an + bv[c]));
+                            rsum += v;
+                            colpart[c] += v;
+                        }
+                        rowerr += fabsf(wave_sum(rsum) - mui[q]);
+                        a_out = lane == rr0 + q ? an : a_out;
+                    }
+                }
+            }
+            if (!STATS && !skip && (((rel + RB) & 63) == 0 || rel + RB >= nrows)) {
+                const int i = i0 + (rel & ~63) + lane;
+                if (i < i1) ab[i] = a_out;
             }
         }
-        if (ch + 1 < nchunk) store_chunk(buf ^ 1);
-        __syncthreads();
     }
     if (skip) return;
 #pragma unroll
     for (int c = 0; c < NCW; ++c) {
         const int j = lane + 64 * c;
-        if (j < d2) T.part[pidx(T, 0, r, b, j)] = colpart[c];
+        T.part[pidx(T, 0, r, b, j)] = colpart[c];  // 0 past d2
     }
     const float lw = STATS ? wave_sum(losspart) : 0.f;
     if (lane == 0) {
@@ -518,7 +688,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
     const int b = blockIdx.x;
     const int st = T.state[b];
     const int K = st ? st : T.n_iter;
-    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2 + (size_t)b * T.d2;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
     float colerr = 0.f;
     for (int j = threadIdx.x; j < T.d2; j += kThreads) {
         float cs = 0.f;
@@ -571,7 +741,11 @@ void row_blocks(int B, int d1, int d2, int c_batched, int *R, int *RBS) {
         unit = kWaves;
     }
     const int maxR = (d1 + unit - 1) / unit;
-    const int r = want < 1 ? 1 : (want > maxR ? maxR : want);
+    int r = want < 1 ? 1 : (want > maxR ? maxR : want);
+    if (W) {
+        const int minR = (d1 + 64 * kSegs - 1) / (64 * kSegs);  // the shared sweep holds <= 64 kSegs rows
+        r = r < minR ? minR : r;
+    }
     int rbs = (d1 + r - 1) / r;
     rbs = (rbs + unit - 1) / unit * unit;
     *RBS = rbs;
@@ -584,16 +758,35 @@ struct Layout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Column registers per lane of the one-row-per-wavefront sweeps (64 lanes x
+// NCW columns), and float4 groups per lane of the streaming sweep; the padded
+// row stride of the workspace covers the widest sweep a shape may take.
+int ncw_bucket(int d2) {
+    const int n = (d2 + 63) / 64;
+    return n <= 4 ? 4 : n <= 8 ? 8 : n <= 13 ? 13 : n <= 16 ? 16 : n <= 32 ? 32 : 64;
+}
+int nc4_bucket(int d2) {
+    const int n = (d2 + 255) / 256;
+    return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
+}
+bool stream_shape(int d2, int c_batched) { return c_batched && d2 % 4 == 0; }
+int padded_width(int d2, int c_batched) {
+    int w = 64 * ncw_bucket(d2);
+    if (stream_shape(d2, c_batched)) w = w > 256 * nc4_bucket(d2) ? w : 256 * nc4_bucket(d2);
+    return w;
+}
+
 Layout layout(int B, int d1, int d2, int c_batched, int *R_out, int *RBS_out, int *JC_out) {
     int R, RBS;
     row_blocks(B, d1, d2, c_batched, &R, &RBS);
     const int JC = (d2 + kMergeThreads - 1) / kMergeThreads;
+    const size_t d2p = padded_width(d2, c_batched);
     Layout L;
     size_t off = 0;
     L.bbuf = off;
-    off = align256(off + sizeof(float) * 2 * (size_t)B * d2);
+    off = align256(off + sizeof(float) * 2 * (size_t)B * d2p);
     L.part = off;
-    off = align256(off + sizeof(float) * 2 * (size_t)R * B * d2);
+    off = align256(off + sizeof(float) * 2 * (size_t)R * B * d2p);
     L.rowerr = off;
     off = align256(off + sizeof(float) * 3 * (size_t)R * B);
     L.lossp = off;
@@ -647,14 +840,26 @@ hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
         [&]() { hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, true>), grid, blk, lds, st, T, 0); });
 }
 
-template <int NCW, int W>
+// Rows per staged chunk and rows per reduction batch of the shared-cost sweep:
+// wide rows keep fewer rows in flight (their plan entries live in registers
+// until the row sum is known).
+template <int NCW>
+struct SharedShape {
+    static constexpr int RB = NCW <= 16 ? 4 : (NCW <= 32 ? 2 : 1);
+    static constexpr int RS = NCW <= 16 ? 8 : (NCW <= 32 ? 4 : 1);
+};
+
+template <int NCW, int W, bool VEC4>
 hipError_t run_shared(const TiledArgs &T, hipStream_t st) {
-    constexpr int RS = (64 / NCW) < 8 ? (64 / NCW) : 8;
+    constexpr int RS = SharedShape<NCW>::RS, RB = SharedShape<NCW>::RB;
     const size_t lds = sizeof(float) * 2 * RS * NCW * 64;
     const dim3 grid(T.R, (T.B + W - 1) / W), blk(64 * W);
     return run_sequence(
-        T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, false>), grid, blk, lds, st, T, k); },
-        [&]() { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, true>), grid, blk, lds, st, T, 0); });
+        T, st,
+        [&](int k) {
+            hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>), grid, blk, lds, st, T, k);
+        },
+        [&]() { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>), grid, blk, lds, st, T, 0); });
 }
 
 template <bool BATCHED>
@@ -667,14 +872,14 @@ hipError_t dispatch(const TiledArgs &T, int ncw, hipStream_t st) {
     return run<64, BATCHED>(T, st);
 }
 
-template <int W>
+template <int W, bool VEC4>
 hipError_t dispatch_shared(const TiledArgs &T, int ncw, hipStream_t st) {
-    if (ncw <= 4) return run_shared<4, W>(T, st);
-    if (ncw <= 8) return run_shared<8, W>(T, st);
-    if (ncw <= 13) return run_shared<13, W>(T, st);
-    if (ncw <= 16) return run_shared<16, W>(T, st);
-    if (ncw <= 32) return run_shared<32, W>(T, st);
-    return run_shared<64, W>(T, st);
+    if (ncw <= 4) return run_shared<4, W, VEC4>(T, st);
+    if (ncw <= 8) return run_shared<8, W, VEC4>(T, st);
+    if (ncw <= 13) return run_shared<13, W, VEC4>(T, st);
+    if (ncw <= 16) return run_shared<16, W, VEC4>(T, st);
+    if (ncw <= 32) return run_shared<32, W, VEC4>(T, st);
+    return run_shared<64, W, VEC4>(T, st);
 }
 
 }  // namespace
@@ -712,6 +917,7 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     T.B = a.B;
     T.d1 = a.d1;
     T.d2 = a.d2;
+    T.d2p = padded_width(a.d2, a.c_batched);
     T.R = R;
     T.RBS = RBS;
     T.JC = JC;
@@ -721,8 +927,10 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     T.tol = a.tol;
     const int ncw = (a.d2 + 63) / 64;
     const int W = shared_width(a.B, a.c_batched);
-    if (W == 8) return dispatch_shared<8>(T, ncw, st);
-    if (W == 4) return dispatch_shared<4>(T, ncw, st);
+    // 16-byte global->LDS copies need 16-byte aligned cost rows.
+    const bool vec4 = a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0;
+    if (W == 8) return vec4 ? dispatch_shared<8, true>(T, ncw, st) : dispatch_shared<8, false>(T, ncw, st);
+    if (W == 4) return vec4 ? dispatch_shared<4, true>(T, ncw, st) : dispatch_shared<4, false>(T, ncw, st);
     if (a.c_batched && a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0) {
         const int nc4 = (a.d2 + 255) / 256;
         if (nc4 <= 1) return run_stream<1>(T, st);

@@ -378,3 +378,37 @@ def test_tiled_variants_early_stop_shared():
     prob = workloads.random_problem(seed=31, B=10, d1=180, d2=200, lam=0.1, n_iter=300, tol=2e-4)
     gpu, ref = check_forward(prob)
     assert np.all(gpu["iters"] < 300)
+
+
+@pytest.mark.parametrize("B,d1,d2,zero_frac", [
+    (8, 300, 500, 0.0),     # 8 column registers per lane, rows reduced four at a time
+    (12, 260, 1000, 0.1),   # 16 column registers, zero masses, a half-idle second group
+    (8, 700, 1500, 0.0),    # 32 column registers, rows reduced two at a time
+    (8, 520, 2100, 0.05),   # 64 column registers, one row at a time
+    (9, 129, 801, 0.0),     # d2 % 4 != 0: 4-byte global->LDS copies
+])
+def test_shared_sweep_shapes(B, d1, d2, zero_frac):
+    """The shared-cost sweep (W problems per work-group, cost rows staged in LDS)
+    at every column-register width it is built for."""
+    prob = workloads.random_problem(seed=B * 7 + d1 + d2, B=B, d1=d1, d2=d2, lam=0.06, n_iter=30,
+                                    zero_frac=zero_frac)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_shared_sweep_multi_segment_rows():
+    """Row blocks of 150 rows (three 64-row segments of row potentials per
+    wavefront) in the shared-cost sweep; oracle on 3 of 512 problems."""
+    prob = workloads.random_problem(seed=77, B=512, d1=1200, d2=200, lam=0.1, n_iter=25)
+    gpu = _gpu(prob)
+    idx = np.array([0, 200, 511])
+    gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx)
+
+
+def test_shared_sweep_small_lambda_exact_rows():
+    """lambda = 1e-3 on a 24x24 grid with a batch of 8 (shared-cost sweep):
+    rows whose shifted sums leave [2^-64, 2^64] take the exact logsumexp."""
+    prob = workloads.make_config(4, B=8, side=24, n_iter=120)
+    gpu, ref = check_forward(prob, merr_atol=1e-4)
+    check_backward(prob, gpu, ref)
