@@ -494,7 +494,9 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     static_assert(RS % RB == 0 && 64 % RS == 0, "chunks must tile 64-row segments");
     extern __shared__ float lds[];  // [2][RS][D2P]
     const int r = blockIdx.x, g = blockIdx.y;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    // The wavefront index is uniform: read it into a scalar register so that
+    // everything derived from it (problem, staging assignments) is scalar.
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int d1 = T.d1, d2 = T.d2;
     const int b_raw = g * W + w;
     // Inactive wavefronts (past the batch, or stopped) keep staging and
@@ -521,10 +523,13 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     const int nrows = i1 - i0;
     const int nchunk = (nrows + RS - 1) / RS;
     const int lpr = (d2 + 64 * VW - 1) / (64 * VW);  // wavefront loads per cost row
+    // Wavefront w issues the loads (row rr, 64-lane segment sg) numbered
+    // w, w + W, w + 2W, ... of the chunk (scalar index arithmetic).
+    const int ld_rr0 = w / lpr, ld_sg0 = w - (w / lpr) * lpr;
     auto issue_chunk = [&](int ch) {
         float *base = lds + (ch & 1) * RS * D2P;
-        for (int q = w; q < RS * lpr; q += W) {  // wavefront-uniform
-            const int rr = q / lpr, sg = q - rr * lpr;
+        int rr = ld_rr0, sg = ld_sg0;
+        for (int q = w; q < RS * lpr; q += W) {
             const int i = i0 + ch * RS + rr;
             const int u = sg * 64 + lane;
             if (i < i1 && u * VW < d2) {
@@ -535,6 +540,7 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                 else
                     __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
             }
+            for (sg += W; sg >= lpr; sg -= lpr) ++rr;
         }
     };
     issue_chunk(0);
@@ -587,18 +593,20 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
             if (!skip) {
                 const int rr0 = rel & 63;
                 float ai[RB], mui[RB], e[RB][NCW], p[RB], rs[RB], f[RB];
+                // Every staged cost value of the batch goes into the plan-entry
+                // registers first (one LDS latency per batch), then each is
+                // turned into its plan entry in place.
+#pragma unroll
+                for (int q = 0; q < RB; ++q)
+#pragma unroll
+                    for (int c = 0; c < NCW; ++c) e[q][c] = cbuf[(rb + q) * D2P + 64 * c];
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
                     ai[q] = uni(a_seg, rr0 + q);
                     mui[q] = uni(mu_seg, rr0 + q);
-                    const float *crow = cbuf + (rb + q) * D2P;
 #pragma unroll
-                    for (int c = 0; c < NCW; ++c) {
-                        // Wide rows: at most 16 staged values in flight, so that the
-                        // plan entries, bv and colpart keep their registers.
-                        if (NCW > 32 && c % 16 == 0 && c > 0) __asm__ volatile("" ::: "memory");
-                        e[q][c] = ex2(__builtin_fmaf(crow[64 * c], ns, ai[q] + bv[c]));
-                    }
+                    for (int c = 0; c < NCW; ++c) e[q][c] = ex2(__builtin_fmaf(e[q][c], ns, ai[q] + bv[c]));
                     p[q] = tree_sum<NCW>(e[q]);
                 }
                 allreduce_rows<RB>(p, rs);
@@ -846,7 +854,7 @@ hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
 template <int NCW>
 struct SharedShape {
     static constexpr int RB = NCW <= 16 ? 4 : (NCW <= 32 ? 2 : 1);
-    static constexpr int RS = NCW <= 16 ? 8 : (NCW <= 32 ? 4 : 1);
+    static constexpr int RS = NCW <= 16 ? 8 : (NCW <= 32 ? 4 : 2);
 };
 
 template <int NCW, int W, bool VEC4>
