@@ -41,6 +41,7 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the onl
 struct TiledArgs {
     const float *mu, *nu, *C;
     float *a;        // [B, d1] base-2 potentials (the alpha output buffer)
+    float *a2;       // [B, d1] second plane of the potentials (streaming sweep: odd iterations), or null
     float *bbuf;     // [2][B, d2p] base-2 column potentials, ping-pong by iteration parity
     float *part;     // [2][R][B, d2p] column partials (plane 1 only for the exact pass)
     float *rowerr;   // [3][R][B] row-error partials: planes 0/1 by iteration parity, 2 for stats
@@ -320,109 +321,6 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-// Cost of a row held in registers (raw C, 4 consecutive columns per float4:
-// element cc is column j = 4 lane + 256 (cc / 4) + cc % 4), scaled on use.
-template <int NCW>
-struct RegCost {
-    const float *v;
-    int lane, d2;
-    float s;
-    __device__ __forceinline__ float operator()(int cc) const {
-        const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
-        return j < d2 ? -s * v[cc] : kPadCost;
-    }
-};
-
-// Sweep for per-sample costs (each C_b read once per iteration, HBM bound):
-// as sk_tiled_sweep, but every lane streams 128-bit non-temporal loads of 4
-// consecutive columns and the next row of the wavefront is in flight while
-// the current one is computed.  Needs d2 % 4 == 0 (16-byte aligned rows).
-template <int NC4, bool STATS>
-__global__ __launch_bounds__(kThreads) void sk_tiled_sweep_stream(TiledArgs T, int k) {
-    constexpr int NCW = 4 * NC4;
-    extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
-    __shared__ float scal[2 * kWaves];
-    const int r = blockIdx.x, b = blockIdx.y;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int d1 = T.d1, d2 = T.d2;
-
-    const int st = T.state[b];
-    if (!STATS) {
-        if (st != 0) return;
-        if (stop_before(T, b, k)) {
-            if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
-            return;
-        }
-    }
-    const int K = STATS ? (st ? st : T.n_iter) : k;
-    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
-    const float *Cb = T.C + (size_t)b * d1 * d2;
-    float *ab = T.a + (size_t)b * d1;
-    const float *mub = T.mu + (size_t)b * d1;
-
-    float bv[NCW], colpart[NCW];
-#pragma unroll
-    for (int cc = 0; cc < NCW; ++cc) {
-        const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
-        bv[cc] = bsrc[j];  // 0 past d2 (padded stride)
-        colpart[cc] = 0.f;
-    }
-    auto load_row = [&](float (&dst)[NCW], int i) {
-        const f4v *row = reinterpret_cast<const f4v *>(Cb + (size_t)i * d2);
-#pragma unroll
-        for (int c = 0; c < NC4; ++c) {
-            const int j0 = 4 * lane + 256 * c;
-            f4v v = {0.f, 0.f, 0.f, 0.f};
-            if (j0 < d2) v = __builtin_nontemporal_load(row + (j0 >> 2));
-            dst[4 * c + 0] = v.x;
-            dst[4 * c + 1] = v.y;
-            dst[4 * c + 2] = v.z;
-            dst[4 * c + 3] = v.w;
-        }
-    };
-    float rowerr = 0.f, losspart = 0.f;
-    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
-    float cur[NCW], nxt[NCW];
-    int i = i0 + w;
-    if (i < i1) load_row(cur, i);
-    for (; i < i1; i += kWaves) {
-        if (i + kWaves < i1) load_row(nxt, i + kWaves);  // in flight during this row
-        const RegCost<NCW> cost{cur, lane, d2, T.s};
-        row_step<NCW, STATS>(cost, ab[i], mub[i], ab + i, bv, colpart, rowerr, losspart, lane);
-#pragma unroll
-        for (int cc = 0; cc < NCW; ++cc) cur[cc] = nxt[cc];
-    }
-
-#pragma unroll
-    for (int cc = 0; cc < NCW; ++cc) {
-        const int j = 4 * lane + 256 * (cc >> 2) + (cc & 3);
-        lds[w * NCW * 64 + j] = colpart[cc];
-    }
-    const float lw = STATS ? wave_sum(losspart) : 0.f;
-    if (lane == 0) {
-        scal[w] = rowerr;
-        scal[kWaves + w] = lw;
-    }
-    __syncthreads();
-    for (int j = threadIdx.x; j < d2; j += kThreads) {
-        float s = 0.f;
-#pragma unroll
-        for (int q = 0; q < kWaves; ++q) s += lds[q * NCW * 64 + j];
-        T.part[pidx(T, 0, r, b, j)] = s;
-    }
-    if (threadIdx.x == 0) {
-        float re = 0.f, lo = 0.f;
-#pragma unroll
-        for (int q = 0; q < kWaves; ++q) {
-            re += scal[q];
-            lo += scal[kWaves + q];
-        }
-        const int plane = STATS ? 2 : (k & 1);
-        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
-        if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
-    }
-}
-
 // Sweep for a cost shared by the batch (Section 4's setting).
 //
 // A work-group of W wavefronts = W problems of group g walks the rows of row
@@ -690,6 +588,310 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     }
 }
 
+// Sweep for per-sample costs (each C_b read once per iteration: HBM bound).
+//
+// Work-group (row block r, problem b) of W wavefronts; wavefront w streams the
+// rows i0 + w, i0 + w + W, ... of its block through its own LDS ring of NB
+// rows, filled by direct 16-byte global->LDS loads, NB - 1 rows ahead of the
+// row it computes: many bytes in flight per CU and no staging registers.  No
+// barrier is needed inside the row loop (each ring belongs to one wavefront;
+// its loads are waited for with vmcnt).  Lane l holds the columns
+// j = 256 c + 4 l + q (c < NC4, q < 4), read from the ring as float4.
+//
+// The merge of the previous sweep's column partials (the v-update of this
+// iteration, fixed order over row blocks) is done at the start by every
+// work-group of the problem, for all columns, so no separate merge kernel
+// runs between sweeps.  Its inputs are double-buffered by iteration parity:
+// sweep k reads partials plane (k-1)&1, row potentials aplane(k-1), and writes
+// plane k&1 and aplane(k) (an exact column logsumexp may read any row).  The
+// same fixed-order sums give every work-group of the problem the same
+// early-stop decision.
+template <int NC4>
+struct StreamShape {
+    static constexpr int W = NC4 <= 8 ? 4 : 2;  // wavefronts per work-group
+    static constexpr int NB = 4;                // ring depth (rows) per wavefront
+};
+
+__device__ __forceinline__ float *aplane(const TiledArgs &T, int k) { return (T.a2 && (k & 1)) ? T.a2 : T.a; }
+
+// Exact logsumexp (base 2) over all rows of a_i + cl_ij for one column of a
+// per-sample cost, reading the row potentials from a.
+__device__ float col_lse_exact_from(const TiledArgs &T, const float *a, int b, int j) {
+    const float *Cb = T.C + (size_t)b * T.d1 * T.d2;
+    float m = neg_inf();
+    for (int i = 0; i < T.d1; ++i) m = fmaxf(m, a[i] - T.s * Cb[(size_t)i * T.d2 + j]);
+    if (m == neg_inf()) return m;
+    float s = 0.f;
+    for (int i = 0; i < T.d1; ++i) s += ex2(a[i] - T.s * Cb[(size_t)i * T.d2 + j] - m);
+    return m + lg2(s);
+}
+
+template <int NC4, bool STATS>
+__global__ __launch_bounds__(64 * StreamShape<NC4>::W) void sk_tiled_sweep_stream(TiledArgs T, int k) {
+    constexpr int W = StreamShape<NC4>::W, NB = StreamShape<NC4>::NB;
+    constexpr int NCW = 4 * NC4, D2S = 256 * NC4, NT = 64 * W;
+    extern __shared__ float lds[];  // [D2S] merged potentials, then [W][NB][D2S] rings, then [W][D2S] partials
+    __shared__ float red[2 * W];
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int d1 = T.d1, d2 = T.d2;
+    const float *Cb = T.C + (size_t)b * d1 * d2;
+    const int st = T.state[b];
+    if (!STATS && st != 0) return;  // stopped after an earlier iteration (work-group uniform)
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+
+    // ---- column potentials of this iteration (v-update folded in for k >= 2)
+    float *bl = lds;  // [D2S], reused by the rings below
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
+    if (!STATS && k >= 2) {
+        const float *bold = T.bbuf + (size_t)((k - 1) & 1) * T.B * T.d2p + (size_t)b * T.d2p;
+        float *bnew = T.bbuf + (size_t)(k & 1) * T.B * T.d2p + (size_t)b * T.d2p;
+        const float *aprev = aplane(T, k - 1) + (size_t)b * d1;
+        // Column sums of the plan after iteration k-1, fixed order over the row
+        // blocks; the loads of QB row blocks x MPT columns are in flight together.
+        constexpr int MPT = (D2S + NT - 1) / NT;        // columns per thread
+        constexpr int QB = MPT >= 64 ? 1 : 64 / MPT;    // row blocks per batch of loads
+        float cs[MPT];
+#pragma unroll
+        for (int m = 0; m < MPT; ++m) cs[m] = 0.f;
+        for (int q0 = 0; q0 < T.R; q0 += QB) {
+            float v[QB][MPT];
+#pragma unroll
+            for (int qq = 0; qq < QB; ++qq)
+#pragma unroll
+                for (int m = 0; m < MPT; ++m) {
+                    const int j = threadIdx.x + NT * m;
+                    v[qq][m] = (q0 + qq < T.R && j < d2) ? T.part[pidx(T, (k - 1) & 1, q0 + qq, b, j)] : 0.f;
+                }
+#pragma unroll
+            for (int qq = 0; qq < QB; ++qq)
+#pragma unroll
+                for (int m = 0; m < MPT; ++m) cs[m] += v[qq][m];
+        }
+        float cerr = 0.f;
+#pragma unroll
+        for (int m = 0; m < MPT; ++m) {
+            const int j = threadIdx.x + NT * m;
+            float v = 0.f;
+            if (j < d2) {
+                const float nuj = T.nu[(size_t)b * d2 + j];
+                cerr += fabsf(cs[m] - nuj);
+                v = neg_inf();
+                if (nuj > 0.f) {
+                    if (cs[m] >= kSumLo && cs[m] <= kSumHi)
+                        v = bold[j] + log2f(nuj) - lg2(cs[m]);
+                    else
+                        v = log2f(nuj) - col_lse_exact_from(T, aprev, b, j);
+                }
+                if (r == 0) bnew[j] = v;
+            }
+            if (j < D2S) bl[j] = v;  // 0 past d2
+        }
+        // Early stop on the marginal error of iterate k-1: its row part from
+        // the previous sweep's row-block partials, its column part just summed.
+        float re = 0.f;
+        if (T.tol > 0.f)
+            for (int q = 0; q < T.R; ++q) re += T.rowerr[((size_t)((k - 1) & 1) * T.R + q) * T.B + b];
+        cerr = wave_sum(cerr);
+        if (lane == 0) red[w] = cerr;
+        __syncthreads();
+        if (T.tol > 0.f) {
+            float err = re;
+#pragma unroll
+            for (int q = 0; q < W; ++q) err += red[q];
+            if (err <= T.tol) {
+                if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
+                return;  // work-group uniform
+            }
+        }
+    } else {
+        for (int j = threadIdx.x; j < D2S; j += NT) bl[j] = bsrc[j];  // 0 past d2 (padded stride)
+        __syncthreads();
+    }
+    float bv[NCW], colpart[NCW];
+#pragma unroll
+    for (int c = 0; c < NC4; ++c) {
+        const f4v v = *reinterpret_cast<const f4v *>(bl + 256 * c + 4 * lane);
+        bv[4 * c + 0] = v.x;
+        bv[4 * c + 1] = v.y;
+        bv[4 * c + 2] = v.z;
+        bv[4 * c + 3] = v.w;
+    }
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) colpart[c] = 0.f;
+    __syncthreads();  // the rings below reuse bl
+
+    // ---- rows of this wavefront: i = i0 + w + W t
+    float *ring = lds + (size_t)w * NB * D2S;
+    if (d2 < D2S)  // padding columns of every ring slot: plan entry exactly 0
+        for (int u = lane; u < NB * (D2S - d2); u += 64) ring[(u / (D2S - d2)) * D2S + d2 + u % (D2S - d2)] = kPadC;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    const int nrow = i0 + w < i1 ? (i1 - i0 - w + W - 1) / W : 0;
+    auto issue_row = [&](int t) {
+        const float *src = Cb + (size_t)(i0 + w + W * t) * d2 + 4 * lane;
+        float *slot = ring + (t % NB) * D2S;
+#pragma unroll
+        for (int c = 0; c < NC4; ++c)
+            if (256 * c + 4 * lane < d2)
+                __builtin_amdgcn_global_load_lds(src + 256 * c, (__attribute__((address_space(3))) void *)(slot + 256 * c),
+                                                 16, 0, 0);
+    };
+    const float *a_in = aplane(T, STATS ? K : k - 1) + (size_t)b * d1;
+    float *a_wr = aplane(T, k) + (size_t)b * d1;
+    const float *mub = T.mu + (size_t)b * d1;
+    // Row potentials and masses of 64 rows per register (lane = row t).
+    float a_s[kSegs], mu_s[kSegs];
+#pragma unroll
+    for (int q = 0; q < kSegs; ++q) {
+        const int t = 64 * q + lane;
+        a_s[q] = t < nrow ? a_in[i0 + w + W * t] : neg_inf();
+        mu_s[q] = t < nrow ? mub[i0 + w + W * t] : 0.f;
+    }
+    for (int t = 0; t < NB - 1 && t < nrow; ++t) issue_row(t);
+    const float ns = -T.s;
+    float rowerr = 0.f, losspart = 0.f;
+    float a_seg = 0.f, mu_seg = 0.f, a_o = 0.f;
+    for (int t = 0; t < nrow; ++t) {
+        if ((t & 63) == 0) {
+            const int sg = t >> 6;
+            a_seg = a_s[0];
+            mu_seg = mu_s[0];
+#pragma unroll
+            for (int q = 1; q < kSegs; ++q) {
+                a_seg = sg == q ? a_s[q] : a_seg;
+                mu_seg = sg == q ? mu_s[q] : mu_seg;
+            }
+            a_o = a_seg;
+        }
+        // Rows t+1 .. t+NB-1 may stay in flight (NC4 loads each); the last
+        // rows of the wavefront wait for everything.
+        if (t + NB - 1 < nrow) {
+            issue_row(t + NB - 1);
+            __asm__ volatile("s_waitcnt vmcnt(%0)" ::"n"(NC4 * (NB - 1)) : "memory");
+        } else {
+            __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        const float *slot = ring + (t % NB) * D2S + 4 * lane;
+        float e[NCW];
+#pragma unroll
+        for (int c = 0; c < NC4; ++c) {
+            const f4v v = *reinterpret_cast<const f4v *>(slot + 256 * c);
+            e[4 * c + 0] = v.x;
+            e[4 * c + 1] = v.y;
+            e[4 * c + 2] = v.z;
+            e[4 * c + 3] = v.w;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        const int tt = t & 63;
+        const float ai = uni(a_seg, tt), mui = uni(mu_seg, tt);
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) e[c] = ex2(__builtin_fmaf(e[c], ns, ai + bv[c]));
+        const float rs = uni(wave_sum(tree_sum<NCW>(e)), 0);
+        float f = 0.f;
+        bool exact = false;
+        if (STATS) {
+            if (mui > 0.f) rowerr += fabsf(rs - mui);
+            __asm__ volatile("" ::: "memory");  // re-read the ring slot
+#pragma unroll
+            for (int c = 0; c < NC4; ++c) {
+                const f4v v = *reinterpret_cast<const f4v *>(slot + 256 * c);
+                losspart = __builtin_fmaf(e[4 * c + 0], v.x * ns, losspart);
+                losspart = __builtin_fmaf(e[4 * c + 1], v.y * ns, losspart);
+                losspart = __builtin_fmaf(e[4 * c + 2], v.z * ns, losspart);
+                losspart = __builtin_fmaf(e[4 * c + 3], v.w * ns, losspart);
+            }
+            f = 1.f;
+        } else if (mui > 0.f) {
+            if (rs >= kSumLo && rs <= kSumHi) {
+                const float an = ai + lg2(mui) - lg2(rs);
+                f = ex2(an - ai);
+                rowerr += fabsf(f * rs - mui);
+                a_o = lane == tt ? an : a_o;
+            } else {
+                exact = true;
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[c], f, colpart[c]);
+        if (!STATS && exact) {
+            // Exact u-update of this row (max, then sum) from the ring slot.
+            float m = neg_inf();
+#pragma unroll
+            for (int c = 0; c < NC4; ++c) {
+                const f4v v = *reinterpret_cast<const f4v *>(slot + 256 * c);
+                m = fmaxf(m, __builtin_fmaf(v.x, ns, bv[4 * c + 0]));
+                m = fmaxf(m, __builtin_fmaf(v.y, ns, bv[4 * c + 1]));
+                m = fmaxf(m, __builtin_fmaf(v.z, ns, bv[4 * c + 2]));
+                m = fmaxf(m, __builtin_fmaf(v.w, ns, bv[4 * c + 3]));
+            }
+            m = wave_max(m);
+            __asm__ volatile("" ::: "memory");
+            float s2 = 0.f;
+#pragma unroll
+            for (int c = 0; c < NC4; ++c) {
+                const f4v v = *reinterpret_cast<const f4v *>(slot + 256 * c);
+                s2 += ex2(__builtin_fmaf(v.x, ns, bv[4 * c + 0]) - m);
+                s2 += ex2(__builtin_fmaf(v.y, ns, bv[4 * c + 1]) - m);
+                s2 += ex2(__builtin_fmaf(v.z, ns, bv[4 * c + 2]) - m);
+                s2 += ex2(__builtin_fmaf(v.w, ns, bv[4 * c + 3]) - m);
+            }
+            s2 = wave_sum(s2);
+            const float an = lg2(mui) - (m + lg2(s2));
+            __asm__ volatile("" ::: "memory");
+            float rsum = 0.f;
+#pragma unroll
+            for (int c = 0; c < NC4; ++c) {
+                const f4v v = *reinterpret_cast<const f4v *>(slot + 256 * c);
+                const float x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float p = ex2(__builtin_fmaf(x[q], ns, an + bv[4 * c + q]));
+                    rsum += p;
+                    colpart[4 * c + q] += p;
+                }
+            }
+            rowerr += fabsf(wave_sum(rsum) - mui);
+            a_o = lane == tt ? an : a_o;
+        }
+        if (!STATS && (((t + 1) & 63) == 0 || t + 1 == nrow)) {
+            const int tw = (t & ~63) + lane;
+            if (tw < nrow) a_wr[i0 + w + W * tw] = a_o;
+        }
+    }
+
+    // ---- combine the wavefronts' column partials (fixed order) and store
+    __syncthreads();  // every ring is drained
+    float *pl = lds;  // [W][D2S]
+#pragma unroll
+    for (int c = 0; c < NC4; ++c) {
+        f4v v = {colpart[4 * c + 0], colpart[4 * c + 1], colpart[4 * c + 2], colpart[4 * c + 3]};
+        *reinterpret_cast<f4v *>(pl + (size_t)w * D2S + 256 * c + 4 * lane) = v;
+    }
+    const float lw = STATS ? wave_sum(losspart) : 0.f;
+    if (lane == 0) {
+        red[w] = rowerr;
+        red[W + w] = lw;
+    }
+    __syncthreads();
+    const int plane = STATS ? 0 : (k & 1);
+    for (int j = threadIdx.x; j < D2S; j += NT) {
+        float s = 0.f;
+#pragma unroll
+        for (int q = 0; q < W; ++q) s += pl[q * D2S + j];
+        T.part[pidx(T, plane, r, b, j)] = s;
+    }
+    if (threadIdx.x == 0) {
+        float re = 0.f, lo = 0.f;
+#pragma unroll
+        for (int q = 0; q < W; ++q) {
+            re += red[q];
+            lo += red[W + q];
+        }
+        T.rowerr[((size_t)(STATS ? 2 : (k & 1)) * T.R + r) * T.B + b] = re;
+        if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
+    }
+}
+
 // Outputs of the returned iterate: marginal error, E^0, natural-log potentials.
 __global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
     __shared__ float red[kWaves];
@@ -706,7 +908,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
     }
     for (int i = threadIdx.x; i < T.d1; i += kThreads) {
         const size_t u = (size_t)b * T.d1 + i;
-        T.alpha_out[u] = T.a[u] * kLn2;
+        T.alpha_out[u] = aplane(T, K)[u] * kLn2;
     }
     colerr = block_sum(colerr, red);
     if (threadIdx.x == 0) {
@@ -735,10 +937,20 @@ int shared_width(int B, int c_batched) {
 // wavefronts, rows per block a multiple of the wavefronts per group.  Shared
 // cost: ~256 (wide rows) or ~512 work-groups, the count of row blocks a
 // multiple of 8 when the rows allow it so that a row block stays on one XCD.
+bool stream_shape(int d2, int c_batched);
+int stream_waves(int d2);
+
 void row_blocks(int B, int d1, int d2, int c_batched, int *R, int *RBS) {
     const int W = shared_width(B, c_batched);
     int want, unit;
-    if (W) {
+    if (stream_shape(d2, c_batched)) {
+        // Streaming sweep: about one work-group per CU, and at most
+        // 64 kSegs rows per wavefront (row potentials held in registers).
+        want = (256 + B - 1) / (B > 0 ? B : 1);
+        const int minR = (d1 + 64 * kSegs * stream_waves(d2) - 1) / (64 * kSegs * stream_waves(d2));
+        want = want < minR ? minR : want;
+        unit = 1;
+    } else if (W) {
         const int G = (B + W - 1) / W;
         const int target = d2 > 1024 ? 256 : 512;
         want = (target + G - 1) / G;
@@ -761,7 +973,7 @@ void row_blocks(int B, int d1, int d2, int c_batched, int *R, int *RBS) {
 }
 
 struct Layout {
-    size_t bbuf, part, rowerr, lossp, colerr, state, total;
+    size_t bbuf, part, rowerr, lossp, colerr, state, a2, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -778,6 +990,8 @@ int nc4_bucket(int d2) {
     return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
 }
 bool stream_shape(int d2, int c_batched) { return c_batched && d2 % 4 == 0; }
+int stream_nc4(int d2) { return (d2 + 255) / 256; }
+int stream_waves(int d2) { return stream_nc4(d2) <= 8 ? 4 : 2; }
 int padded_width(int d2, int c_batched) {
     int w = 64 * ncw_bucket(d2);
     if (stream_shape(d2, c_batched)) w = w > 256 * nc4_bucket(d2) ? w : 256 * nc4_bucket(d2);
@@ -803,6 +1017,8 @@ Layout layout(int B, int d1, int d2, int c_batched, int *R_out, int *RBS_out, in
     off = align256(off + sizeof(float) * (size_t)B * JC);
     L.state = off;
     off = align256(off + sizeof(int32_t) * (size_t)B);
+    L.a2 = off;
+    if (stream_shape(d2, c_batched)) off = align256(off + sizeof(float) * (size_t)B * d1);
     L.total = off;
     if (R_out) *R_out = R;
     if (RBS_out) *RBS_out = RBS;
@@ -839,13 +1055,30 @@ hipError_t run(const TiledArgs &T, hipStream_t st) {
         [&]() { hipLaunchKernelGGL((sk_tiled_sweep<NCW, true, BATCHED>), grid, blk, lds, st, T, 0); });
 }
 
+// Streaming sweep sequence: the merges are folded into the sweeps.
 template <int NC4>
 hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
-    const size_t lds = sizeof(float) * kWaves * 4 * NC4 * 64;
-    const dim3 grid(T.R, T.B), blk(kThreads);
-    return run_sequence(
-        T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, false>), grid, blk, lds, st, T, k); },
-        [&]() { hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, true>), grid, blk, lds, st, T, 0); });
+    constexpr int W = StreamShape<NC4>::W, NB = StreamShape<NC4>::NB;
+    const size_t lds = sizeof(float) * W * NB * 256 * NC4;
+    static bool attr = false;  // rings above 64 KB need the larger dynamic LDS limit
+    if (!attr) {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_stream<NC4, false>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_stream<NC4, true>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        attr = true;
+    }
+    const dim3 grid(T.R, T.B), blk(64 * W);
+    hipLaunchKernelGGL(sk_tiled_init, dim3(512), dim3(kThreads), 0, st, T);
+    if (T.n_iter > 0) {
+        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+        hipLaunchKernelGGL(sk_tiled_merge<true>, dim3(T.JC, T.B), dim3(kMergeThreads), 0, st, T, 0);
+        for (int k = 1; k <= T.n_iter; ++k)
+            hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, false>), grid, blk, lds, st, T, k);
+    }
+    hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, true>), grid, blk, lds, st, T, 0);
+    hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), dim3(kThreads), 0, st, T);
+    return hipGetLastError();
 }
 
 // Rows per staged chunk and rows per reduction batch of the shared-cost sweep:
@@ -911,6 +1144,7 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     T.nu = a.nu;
     T.C = a.C;
     T.a = a.alpha;
+    T.a2 = nullptr;
     T.bbuf = reinterpret_cast<float *>(base + L.bbuf);
     T.part = reinterpret_cast<float *>(base + L.part);
     T.rowerr = reinterpret_cast<float *>(base + L.rowerr);
@@ -939,13 +1173,26 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     const bool vec4 = a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0;
     if (W == 8) return vec4 ? dispatch_shared<8, true>(T, ncw, st) : dispatch_shared<8, false>(T, ncw, st);
     if (W == 4) return vec4 ? dispatch_shared<4, true>(T, ncw, st) : dispatch_shared<4, false>(T, ncw, st);
-    if (a.c_batched && a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0) {
-        const int nc4 = (a.d2 + 255) / 256;
-        if (nc4 <= 1) return run_stream<1>(T, st);
-        if (nc4 <= 2) return run_stream<2>(T, st);
-        if (nc4 <= 4) return run_stream<4>(T, st);
-        if (nc4 <= 8) return run_stream<8>(T, st);
-        return run_stream<16>(T, st);
+    if (stream_shape(a.d2, a.c_batched) && ((uintptr_t)a.C % 16) == 0) {
+        T.a2 = reinterpret_cast<float *>(base + L.a2);
+        switch (stream_nc4(a.d2)) {
+            case 1: return run_stream<1>(T, st);
+            case 2: return run_stream<2>(T, st);
+            case 3: return run_stream<3>(T, st);
+            case 4: return run_stream<4>(T, st);
+            case 5: return run_stream<5>(T, st);
+            case 6: return run_stream<6>(T, st);
+            case 7: return run_stream<7>(T, st);
+            case 8: return run_stream<8>(T, st);
+            case 9: return run_stream<9>(T, st);
+            case 10: return run_stream<10>(T, st);
+            case 11: return run_stream<11>(T, st);
+            case 12: return run_stream<12>(T, st);
+            case 13: return run_stream<13>(T, st);
+            case 14: return run_stream<14>(T, st);
+            case 15: return run_stream<15>(T, st);
+            default: return run_stream<16>(T, st);
+        }
     }
     if (a.c_batched) return dispatch<true>(T, ncw, st);
     return dispatch<false>(T, ncw, st);

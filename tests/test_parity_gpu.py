@@ -412,3 +412,35 @@ def test_shared_sweep_small_lambda_exact_rows():
     prob = workloads.make_config(4, B=8, side=24, n_iter=120)
     gpu, ref = check_forward(prob, merr_atol=1e-4)
     check_backward(prob, gpu, ref)
+
+
+def test_stream_early_stop_per_sample():
+    """Per-sample costs streamed through LDS rings: the merge folded into the
+    next sweep takes the same per-sample stop decision in every row block."""
+    prob = workloads.random_problem(seed=41, B=5, d1=300, d2=400, lam=0.1, n_iter=400, c_batched=True, tol=1e-4)
+    gpu, ref = check_forward(prob)
+    _say(f"   iters {gpu['iters'].tolist()}")
+    assert np.all(gpu["iters"] < 400)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+@pytest.mark.parametrize("d1,d2", [(150, 4000), (100, 2400), (300, 512)])
+def test_stream_widths(d1, d2):
+    """Streaming sweep at 16 and 10 float4 groups per lane (two wavefronts per
+    work-group) and at 2 groups with one-row blocks (B = 1: some wavefronts
+    get no row)."""
+    B = 1 if d2 == 512 else 2
+    prob = workloads.random_problem(seed=d1 + d2, B=B, d1=d1, d2=d2, lam=0.07, n_iter=30, c_batched=True,
+                                    zero_frac=0.05)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_stream_small_lambda_exact_paths():
+    """lambda = 1e-3 on a per-sample 1-D grid cost: rows and columns whose
+    shifted sums leave [2^-64, 2^64] take the exact logsumexp in the ring
+    sweep and in the folded merge (which reads the previous potentials plane)."""
+    prob = workloads.random_problem(seed=43, B=2, d1=300, d2=304, lam=1e-3, n_iter=200, c_batched=True,
+                                    cost="grid1d")
+    gpu, ref = check_forward(prob, merr_atol=1e-4)
+    check_backward(prob, gpu, ref)
