@@ -145,8 +145,15 @@ __global__ __launch_bounds__(kMergeThreads) void sk_tiled_merge(TiledArgs T, int
             if (nuj > 0.f) bnew = log2f(nuj) - (M + lg2(S));
             T.bbuf[(size_t)1 * T.B * T.d2p + (size_t)b * T.d2p + j] = bnew;
         } else {
+            // Fixed-order sum over the row blocks; 8 loads in flight at a time.
             float cs = 0.f;
-            for (int r = 0; r < T.R; ++r) cs += T.part[pidx(T, 0, r, b, j)];
+            for (int r0 = 0; r0 < T.R; r0 += 8) {
+                float v[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v[q] = r0 + q < T.R ? T.part[pidx(T, 0, r0 + q, b, j)] : 0.f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) cs += v[q];
+            }
             err = fabsf(cs - nuj);
             if (nuj > 0.f) {
                 const float bold = T.bbuf[(size_t)(k & 1) * T.B * T.d2p + (size_t)b * T.d2p + j];
@@ -341,10 +348,11 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 constexpr float kPadC = 1.0e30f;  // raw cost of padding cells: exp underflows to 0, 0 * cl stays finite
 constexpr int kSegs = 4;          // row blocks of the shared-cost sweep hold at most 64 kSegs rows
 
-// All-reduce of RB per-lane partials (RB = 1, 2 or 4); every lane gets the
-// same bits.  Packing: a permlane32 swap pairs (p0, p1) so that lanes < 32
-// carry p0's half-sums and lanes >= 32 p1's; a permlane16 swap then packs
-// four vectors into the four 16-lane rows (p0, p2, p1, p3).
+// All-reduce of RB per-lane partials (RB = 1, 2 or 4).  Packing: a permlane32
+// swap pairs (p0, p1) so that lanes < 32 carry p0's half-sums and lanes >= 32
+// p1's; a permlane16 swap then packs four vectors into the four 16-lane rows
+// (p0, p2, p1, p3); the 16-lane DPP stages finish every row at once, each
+// lane of a row with the same bits.
 __device__ __forceinline__ LanePair swap32x(float x, float y) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
     return {__uint_as_float(r[0]), __uint_as_float(r[1])};
@@ -360,28 +368,36 @@ __device__ __forceinline__ float sum16(float v) {  // all-reduce within each 16-
 __device__ __forceinline__ float uni(float v, int lane) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
+// The result stays in the packed layout: the 16-lane group (lane >> 4) holds
+// the sum of row row_of_lane(lane); lane_of_row(q) is the first lane holding
+// row q.
 template <int RB>
-__device__ __forceinline__ void allreduce_rows(const float (&p)[RB], float (&s)[RB]) {
+__device__ __forceinline__ float allreduce_rows_packed(const float (&p)[RB]) {
     if constexpr (RB == 1) {
-        s[0] = uni(wave_sum(p[0]), 0);
+        return wave_sum(p[0]);
     } else if constexpr (RB == 2) {
         const LanePair a = swap32x(p[0], p[1]);
-        float v = a.lo + a.hi;
-        const LanePair b = swap16(v);
-        v = sum16(b.lo + b.hi);
-        s[0] = uni(v, 0);
-        s[1] = uni(v, 32);
+        const LanePair b = swap16(a.lo + a.hi);
+        return sum16(b.lo + b.hi);
     } else {
         static_assert(RB == 4, "RB must be 1, 2 or 4");
         const LanePair a = swap32x(p[0], p[1]);
         const LanePair b = swap32x(p[2], p[3]);
         const LanePair c = swap16x(a.lo + a.hi, b.lo + b.hi);
-        const float v = sum16(c.lo + c.hi);
-        s[0] = uni(v, 0);
-        s[2] = uni(v, 16);
-        s[1] = uni(v, 32);
-        s[3] = uni(v, 48);
+        return sum16(c.lo + c.hi);
     }
+}
+template <int RB>
+__device__ __forceinline__ int row_of_lane(int lane) {
+    return RB == 4 ? ((lane >> 4) & 1) * 2 + (lane >> 5) : (RB == 2 ? lane >> 5 : 0);
+}
+template <int RB>
+__device__ __forceinline__ int lane_of_row(int q) {
+    return RB == 4 ? (q & 1) * 32 + (q >> 1) * 16 : (RB == 2 ? 32 * q : 0);
+}
+// Value of register v in lane src (any lane, per-lane index).
+__device__ __forceinline__ float lane_get(float v, int src) {
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
 }
 
 template <int NCW, int W, int RS, int RB, bool VEC4, bool STATS>
@@ -412,9 +428,11 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     }
     if (!__syncthreads_or(!skip)) return;
 
-    // Every LDS word starts finite (padding cost), so rows past the block and
-    // columns past d2 give plan entries of exactly 0.
-    for (int u = threadIdx.x; u < 2 * RS * D2P; u += NT) lds[u] = kPadC;
+    // Columns past d2 hold the padding cost (plan entries exactly 0); loads
+    // never touch them.  Rows past the block are never read (see below).
+    if (d2 < D2P)
+        for (int u = threadIdx.x; u < 2 * RS * (D2P - d2); u += NT)
+            lds[(u / (D2P - d2)) * D2P + d2 + u % (D2P - d2)] = kPadC;
     __syncthreads();
 
     const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
@@ -490,55 +508,66 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
             }
             if (!skip) {
                 const int rr0 = rel & 63;
-                float ai[RB], mui[RB], e[RB][NCW], p[RB], rs[RB], f[RB];
+                float ai[RB], e[RB][NCW], p[RB], f[RB];
                 // Every staged cost value of the batch goes into the plan-entry
                 // registers first (one LDS latency per batch), then each is
-                // turned into its plan entry in place.
+                // turned into its plan entry in place.  Rows past the block
+                // (a = -inf) read the batch's first row, which is staged.
 #pragma unroll
-                for (int q = 0; q < RB; ++q)
+                for (int q = 0; q < RB; ++q) {
+                    const int rq = rel + q < nrows ? rb + q : rb;
 #pragma unroll
-                    for (int c = 0; c < NCW; ++c) e[q][c] = cbuf[(rb + q) * D2P + 64 * c];
+                    for (int c = 0; c < NCW; ++c) e[q][c] = cbuf[rq * D2P + 64 * c];
+                }
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
                     ai[q] = uni(a_seg, rr0 + q);
-                    mui[q] = uni(mu_seg, rr0 + q);
 #pragma unroll
                     for (int c = 0; c < NCW; ++c) e[q][c] = ex2(__builtin_fmaf(e[q][c], ns, ai[q] + bv[c]));
                     p[q] = tree_sum<NCW>(e[q]);
                 }
-                allreduce_rows<RB>(p, rs);
-                bool exact[RB];
+                // Row updates of the batch, one row per 16-lane group (the
+                // all-reduce's packed layout): each lane fetches its row's
+                // potential and mass from the segment registers.
+                const float rsv = allreduce_rows_packed<RB>(p);
+                const int src = rr0 + row_of_lane<RB>(lane);
+                const float av = lane_get(a_seg, src), muv = lane_get(mu_seg, src);
+                bool exact_any = false;
+                if (STATS) {
+                    rowerr += muv > 0.f ? fabsf(rsv - muv) : 0.f;
 #pragma unroll
-                for (int q = 0; q < RB; ++q) {
-                    exact[q] = false;
-                    if (STATS) {
-                        const float *crow = cbuf + (rb + q) * D2P;
-                        if (mui[q] > 0.f) rowerr += fabsf(rs[q] - mui[q]);
+                    for (int q = 0; q < RB; ++q) {
+                        const int rq = rel + q < nrows ? rb + q : rb;
                         __asm__ volatile("" ::: "memory");  // re-read the staged row
 #pragma unroll
-                        for (int c = 0; c < NCW; ++c) losspart = __builtin_fmaf(e[q][c], crow[64 * c] * ns, losspart);
+                        for (int c = 0; c < NCW; ++c)
+                            losspart = __builtin_fmaf(e[q][c], cbuf[rq * D2P + 64 * c] * ns, losspart);
                         f[q] = 1.f;
-                    } else if (!(mui[q] > 0.f)) {  // zero mass (or past the block): a_i = -inf, plan row 0
-                        f[q] = 0.f;
-                    } else if (rs[q] >= kSumLo && rs[q] <= kSumHi) {
-                        const float an = ai[q] + uni(lmu_seg, rr0 + q) - lg2(rs[q]);
-                        f[q] = ex2(an - ai[q]);
-                        rowerr += fabsf(f[q] * rs[q] - mui[q]);
-                        a_out = lane == rr0 + q ? an : a_out;
-                    } else {
-                        f[q] = 0.f;  // this row is redone exactly below
-                        exact[q] = true;
                     }
+                } else {
+                    const bool inr = rsv >= kSumLo && rsv <= kSumHi;
+                    const bool upd = muv > 0.f && inr;
+                    const float an = av + lane_get(lmu_seg, src) - lg2(rsv);
+                    const float fv = upd ? ex2(an - av) : 0.f;
+                    rowerr += upd ? fabsf(fv * rsv - muv) : 0.f;
+                    exact_any = __any(muv > 0.f && !inr);
+#pragma unroll
+                    for (int q = 0; q < RB; ++q) f[q] = uni(fv, lane_of_row<RB>(q));
+                    // lane rr0 + q takes row q's new potential
+                    const int dq = lane - rr0;
+                    const float got = lane_get(upd ? an : av, lane_of_row<RB>(dq >= 0 && dq < RB ? dq : 0));
+                    a_out = dq >= 0 && dq < RB ? got : a_out;
                 }
 #pragma unroll
                 for (int q = 0; q < RB; ++q)
 #pragma unroll
                     for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[q][c], f[q], colpart[c]);
-                if (!STATS) {
+                if (!STATS && exact_any) {
 #pragma unroll
                     for (int q = 0; q < RB; ++q) {
-                        if (!exact[q]) continue;
+                        const float mui = uni(mu_seg, rr0 + q), rsq = uni(rsv, lane_of_row<RB>(q));
+                        if (!(mui > 0.f) || (rsq >= kSumLo && rsq <= kSumHi)) continue;
                         // The shifted row sum left [2^-64, 2^64]: exact u-update
                         // of this row (max, then sum) from the staged cost, and
                         // its plan entries rebuilt from the new potential.
@@ -563,7 +592,7 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                             rsum += v;
                             colpart[c] += v;
                         }
-                        rowerr += fabsf(wave_sum(rsum) - mui[q]);
+                        rowerr += lane == lane_of_row<RB>(q) ? fabsf(wave_sum(rsum) - mui) : 0.f;
                         a_out = lane == rr0 + q ? an : a_out;
                     }
                 }
@@ -581,9 +610,14 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
         T.part[pidx(T, 0, r, b, j)] = colpart[c];  // 0 past d2
     }
     const float lw = STATS ? wave_sum(losspart) : 0.f;
+    // rowerr is per 16-lane group (one batch row each): add the groups' totals
+    // in a fixed order.
+    float re = 0.f;
+#pragma unroll
+    for (int q = 0; q < RB; ++q) re += uni(rowerr, lane_of_row<RB>(q));
     if (lane == 0) {
         const int plane = STATS ? 2 : (k & 1);
-        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = rowerr;
+        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
         if (STATS) T.lossp[(size_t)r * T.B + b] = lw;
     }
 }
