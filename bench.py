@@ -34,12 +34,24 @@ PEAK_EXP_TS = 256 * 4 * 8 * 2.4e9 / 1e12
 PEAK_FP32_MFMA = 157.3
 PEAK_FP32_VALU = 157.3
 
-# Resident kernels: the first choice for a shape (shared cost: matrix cores;
-# per-sample cost: plain form on the vector ALU) and the source it is built from.
+# Resident kernels: the first choice for a shape and the source it is built
+# from.  A shared symmetric cost with d1 = d2 <= 104: one work-group per problem
+# on the vector ALU; another shared cost: matrix cores; a per-sample cost: the
+# plain form on the vector ALU.
 RESIDENT_KERNELS = {
-    False: ("sk_resident_mfma_kernel", "sk_resident_mfma.hip", "mfma", PEAK_FP32_MFMA),
-    True: ("sk_resident_plain_kernel", "sk_resident_plain.hip", "alu", PEAK_FP32_VALU),
+    "sym": ("sk_resident_sym_kernel", "sk_resident_sym.hip", "alu", PEAK_FP32_VALU),
+    "shared": ("sk_resident_mfma_kernel", "sk_resident_mfma.hip", "mfma", PEAK_FP32_MFMA),
+    "batched": ("sk_resident_plain_kernel", "sk_resident_plain.hip", "alu", PEAK_FP32_VALU),
 }
+
+
+def resident_kind(prob):
+    if prob.c_batched:
+        return "batched"
+    C = prob.C[0]
+    if prob.d1 == prob.d2 <= 104 and np.array_equal(C.view(np.uint32), C.T.view(np.uint32)):
+        return "sym"
+    return "shared"
 
 WORKLOAD_NAMES = {
     1: "tiny: B=4, d1=d2=10, shared 1-D squared cost, lambda=0.1, 100 iterations + backward",
@@ -174,13 +186,13 @@ def main():
 
     # Roofline of the dominant kernel.
     if regime == 1:
-        # Resident regime: the plain-form kernel solves every problem (the
-        # log-domain fallback launched after it finds nothing to do).  Its
+        # Resident regime: the first-choice plain-form kernel solves every
+        # problem (the fallbacks launched after it find nothing to do).  Its
         # duration alone is taken with events around launches of that kernel
         # only, on the stream the library launches on.  Algorithmic work: two
         # matrix-vector products (4*d1*d2 flops) per iteration, plus the first
         # v-update and the three products of the closing measurement (6*d1*d2).
-        kname, kfile, bound, peak = RESIDENT_KERNELS[bool(prob.c_batched)]
+        kname, kfile, bound, peak = RESIDENT_KERNELS[resident_kind(prob)]
         os.environ["SK_RESIDENT_FORM"] = "plain"
         kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
         for k in range(args.steps):

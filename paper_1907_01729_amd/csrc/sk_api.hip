@@ -23,18 +23,44 @@ sk_status check_problem(const sk_problem *p) {
     return SK_OK;
 }
 
-// Which resident kernel runs (diagnostic switch, environment variable
-// SK_RESIDENT_FORM): "log" forces the log-domain kernel, "plain" runs the
-// plain-form kernel alone (problems it cannot take stay at iters = -1),
-// anything else the plain form with the log-domain kernel as its fallback.
-constexpr int kFormAuto = 0, kFormLog = 1, kFormPlain = 2;
+// Which resident kernels run (diagnostic switch, environment variable
+// SK_RESIDENT_FORM): "log" forces the log-domain kernel; "plain" runs the
+// first-choice plain-form kernel alone (problems it hands over stay at
+// iters = -1 or -2); "nosym" skips the symmetric-cost kernel; anything else
+// runs the plain form with its fallbacks.
+constexpr int kFormAuto = 0, kFormLog = 1, kFormPlain = 2, kFormNoSym = 3;
 
 int resident_form() {
     const char *e = getenv("SK_RESIDENT_FORM");
     if (!e) return kFormAuto;
     if (!strcmp(e, "log")) return kFormLog;
     if (!strcmp(e, "plain")) return kFormPlain;
+    if (!strcmp(e, "nosym")) return kFormNoSym;
     return kFormAuto;
+}
+
+// Resident regime.  First choice: the symmetric-cost kernel (shared cost,
+// d1 = d2 <= 104), else the matrix-core kernel (shared cost), else the
+// per-sample plain-form kernel.  Each hands over what it cannot solve: the
+// symmetric kernel to the matrix-core kernel (iters = -2), every plain form
+// to the log-domain kernel (iters = -1).  Launches on one stream, in order.
+hipError_t launch_resident_regime(sk::FwdArgs a, int form, hipStream_t s) {
+    if (form == kFormLog) return sk::launch_resident(a, s);
+    hipError_t e = hipSuccess;
+    bool ran;
+    if (form != kFormNoSym && sk::launch_resident_sym(a, s, &e)) {
+        ran = true;
+        if (e == hipSuccess && form != kFormPlain) {
+            a.only_flagged = 2;
+            if (!sk::launch_resident_mfma(a, s, &e)) return hipErrorInvalidValue;  // takes every shape the first takes
+        }
+    } else {
+        ran = sk::launch_resident_mfma(a, s, &e) || sk::launch_resident_plain(a, s, &e);
+    }
+    if (!ran) return sk::launch_resident(a, s);
+    if (e != hipSuccess || form == kFormPlain) return e;
+    a.only_flagged = 1;
+    return sk::launch_resident(a, s);
 }
 
 }  // namespace
@@ -101,15 +127,7 @@ sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu
     if (!sk::resident_fits(p->d1, p->d2)) {
         e = sk::launch_tiled(a, workspace, s);
     } else {
-        const int form = resident_form();
-        if (form != kFormLog && (sk::launch_resident_mfma(a, s, &e) || sk::launch_resident_plain(a, s, &e))) {
-            if (e == hipSuccess && form == kFormAuto) {
-                a.only_flagged = 1;
-                e = sk::launch_resident(a, s);
-            }
-        } else {
-            e = sk::launch_resident(a, s);
-        }
+        e = launch_resident_regime(a, resident_form(), s);
     }
     return e == hipSuccess ? SK_OK : SK_ERR_HIP;
 }

@@ -19,7 +19,8 @@ struct FwdArgs {
     float lambda, tol;
     float s;  // log2(e) / lambda
     // Set when a plain-form launch ran first: solve only the problems it
-    // marked with iters = -1 and leave the others untouched.
+    // marked with iters = -only_flagged (-1: out of the plain form's range;
+    // -2: the cost is not symmetric) and leave the others untouched.
     int only_flagged;
 };
 
@@ -41,7 +42,12 @@ hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
 // cannot keep in range come back with iters = -1.
 bool launch_resident_plain(const FwdArgs &a, hipStream_t st, hipError_t *err);
 // Same contract; a cost shared by the batch only, products on the matrix cores.
+// With only_flagged = 2 it solves the problems marked iters = -2.
 bool launch_resident_mfma(const FwdArgs &a, hipStream_t st, hipError_t *err);
+// Same contract; a shared cost with d1 = d2 <= 104, one wavefront per problem
+// on the vector ALU.  A cost that is not symmetric marks every problem with
+// iters = -2 (for the matrix-core kernel).
+bool launch_resident_sym(const FwdArgs &a, hipStream_t st, hipError_t *err);
 
 // The tiled sweep keeps a whole cost row in one wavefront's registers.
 constexpr int kTiledMaxD2 = 4096;

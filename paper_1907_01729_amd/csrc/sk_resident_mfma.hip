@@ -137,7 +137,10 @@ __global__ __launch_bounds__(256) void sk_resident_mfma_kernel(FwdArgs A) {
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int n = l & 3;
     const int b = 4 * blockIdx.x + n;  // this lane's problem
-    const bool real = b < A.B;
+    // only_flagged == 2: the symmetric-cost kernel ran first and handed over
+    // the problems it marked with iters = -2; the others are left untouched.
+    const bool real = b < A.B && (A.only_flagged != 2 || A.iters[b] == -2);
+    if (A.only_flagged == 2 && !__any(real)) return;  // one verdict for the work-group: its lanes span its 4 problems
     const int d1 = A.d1, d2 = A.d2;
     const float s = A.s;
     const float *C = A.C;
@@ -160,7 +163,7 @@ __global__ __launch_bounds__(256) void sk_resident_mfma_kernel(FwdArgs A) {
     mx = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
     mn = fminf(fminf(red[1][0], red[1][1]), fminf(red[1][2], red[1][3]));
     if (!(mx - mn <= kRangeBits)) {
-        if (threadIdx.x < 4 && 4 * blockIdx.x + (int)threadIdx.x < A.B) A.iters[4 * blockIdx.x + threadIdx.x] = -1;
+        if (threadIdx.x < 4 && real) A.iters[b] = -1;  // lanes 0..3 hold problems 0..3
         return;
     }
     const float clmax = mx;

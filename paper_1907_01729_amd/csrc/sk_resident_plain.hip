@@ -113,13 +113,13 @@ __global__ __launch_bounds__(64 * H) __attribute__((amdgpu_waves_per_eu(2))) voi
 #pragma unroll
         for (int t = 0; t < N; ++t) {
             const int j = q + 8 * t;
+            // Cells outside the problem hold -inf (K = 0 there), so no mask
+            // per cell has to stay alive past this loop.
             const bool v = i < d1 && j < d2;
-            const float c = v ? -s * Cb[(size_t)i * d2 + j] : 0.f;
+            const float c = v ? -s * Cb[(size_t)i * d2 + j] : neg_inf();
             KA[r][t] = c;
-            if (v) {
-                mx = fmaxf(mx, c);
-                mn = fminf(mn, c);
-            }
+            mx = fmaxf(mx, c);
+            mn = fminf(mn, v ? c : __builtin_inff());
         }
     }
     mx = wave_max(mx);
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(64 * H) __attribute__((amdgpu_waves_per_eu(2))) voi
     for (int r = 0; r < NR; ++r) {
         const int i = H * (p + 8 * r) + h;
 #pragma unroll
-        for (int t = 0; t < N; ++t) KA[r][t] = (i < d1 && q + 8 * t < d2) ? ex2(KA[r][t] - clmax) : 0.f;
+        for (int t = 0; t < N; ++t) KA[r][t] = ex2(KA[r][t] - clmax);
     }
     float KB[NR][N];  // KB[t][r] = K[q + 8r, H(p + 8t) + h]
 #pragma unroll
@@ -299,10 +299,13 @@ __global__ __launch_bounds__(64 * H) __attribute__((amdgpu_waves_per_eu(2))) voi
         float s0 = 0.f, l0 = 0.f;
 #pragma unroll
         for (int t = 0; t < N; ++t) {
+            // K is 0 on cells outside the problem: read a clamped (in-bounds)
+            // cost there instead of keeping a mask per cell alive.
             const int j = q + 8 * t;
+            const int ic = i < d1 ? i : d1 - 1, jc = j < d2 ? j : d2 - 1;
             const float kv = KA[r][t] * V[t];
             s0 += kv;
-            if (i < d1 && j < d2) l0 = __builtin_fmaf(kv, -s * Cb[(size_t)i * d2 + j], l0);
+            l0 = __builtin_fmaf(kv, -s * Cb[(size_t)ic * d2 + jc], l0);
         }
         const float R = sum_q(s0);
         const float Lr = sum_q(l0);

@@ -1,0 +1,431 @@
+// sk_resident_sym.hip -- a symmetric cost shared by the batch, d1 = d2 <= 104
+// (the label-space case: one set of points on both sides): one work-group of
+// two wavefronts per problem, the plain form of eq. (sk_plain) on the vector
+// ALU.
+//
+// With K = 2^(cl - clmax) (cl = -C log2(e)/lambda, clmax = max cl) the
+// iteration is R = K V, U = mu / R, S = K^T U, V = nu / S, from u^0 = 1 on
+// the support of mu: the same iterates, range guards and outputs as the
+// matrix-core kernel (alpha = ln2 log2 U, beta = ln2 (log2 V - clmax)), so the
+// potentials equal the log-domain iterates up to rounding.
+//
+// Lane l = p + 8q (p = l & 7, q = l >> 3) of wavefront w holds K[p + 8r][q + 8t]
+// for its row blocks r in [w H, w H + H) and every column block t < NC
+// (8 NC >= d, H = ceil(NC / 2)).  A product K w takes w "by columns"
+// (register t of lane (p, q) holds w[q + 8t], read from LDS), forms per-lane
+// partial row sums over t, and reduces them over the 8 lanes q (lane bits 5,
+// 4, 3) by a reduce-scatter: at each step a lane keeps half of its rows and
+// adds its partner's copy of the same rows (v_permlane32_swap,
+// v_permlane16_swap, then DPP row_ror:8), so that each row total ends in one
+// lane.  The update runs on that lane only and publishes the new scaling to
+// LDS for the next product; one barrier per product.  Because K is symmetric,
+// K^T U is the same product as K U, so one register copy of K serves both
+// passes.
+//
+// The kernel verifies the symmetry of the cost first, pair by pair (bit
+// equality); a cost that is not symmetric marks every problem with iters = -2
+// for the matrix-core kernel, launched next.  A problem outside the plain
+// form's range gets iters = -1 (the log-domain kernel takes it), at the start
+// or as soon as a guard fails: a sum R_i, S_j outside [2^-64, 2^64] or a
+// scaling U_i, V_j outside [2^-100, 2^100] on the supports.
+#include "sk_device.h"
+#include "sk_internal.h"
+
+namespace sk {
+namespace {
+
+constexpr float kLo = 5.42101086242752217e-20f;   // 2^-64
+constexpr float kHi = 1.84467440737095516e19f;    // 2^64
+constexpr float kSMin = 7.8886090522101181e-31f;  // 2^-100
+constexpr float kSMax = 1.2676506002282294e30f;   // 2^100
+constexpr float kRangeBits = 64.f;
+
+__device__ __forceinline__ bool sum_ok(float x) { return x >= kLo && x <= kHi; }
+__device__ __forceinline__ bool scale_ok(float x) { return x >= kSMin && x <= kSMax; }
+
+// ---- reduce-scatter bookkeeping (compile time) ----
+// A step over N entries: the low lane keeps entries [0, H), the high lane
+// [H, N), H = ceil(N / 2); a step over a single entry is an all-reduce (both
+// lanes keep it, the low lane owns it).
+constexpr int half_up(int n) { return (n + 1) / 2; }
+template <int NC>
+struct Scatter {
+    static constexpr int N1 = half_up(NC), N2 = half_up(N1), S = half_up(N2);  // S: slots per lane
+};
+
+// Row index r (rows p + 8r) held by slot s of the lanes with column block q
+// (lane bits 5, 4, 3 = q bits 2, 1, 0), or -1 when the slot holds no row of
+// its own (padding or a duplicate).
+constexpr int scatter_row(int NC, int q, int s) {
+    int n = NC, base = 0, cnt = NC;
+    const int bits[3] = {(q >> 2) & 1, (q >> 1) & 1, q & 1};
+    for (int k = 0; k < 3; ++k) {
+        if (n == 1) {
+            if (bits[k]) return -1;
+            continue;
+        }
+        const int h = half_up(n);
+        if (bits[k]) {
+            base += h;
+            cnt = cnt > h ? cnt - h : 0;
+        } else {
+            cnt = cnt < h ? cnt : h;
+        }
+        n = h;
+    }
+    return s < cnt ? base + s : -1;
+}
+
+// One reduce-scatter step over lane bit BIT (5, 4 or 3).
+template <int BIT, int N>
+__device__ __forceinline__ void scatter_step(const float (&v)[N], float (&w)[half_up(N)], bool hi) {
+    constexpr int H = half_up(N);
+    if constexpr (N == 1) {
+        if constexpr (BIT == 5) {
+            const LanePair x = swap32(v[0]);
+            w[0] = x.lo + x.hi;
+        } else if constexpr (BIT == 4) {
+            const LanePair x = swap16(v[0]);
+            w[0] = x.lo + x.hi;
+        } else {
+            w[0] = v[0] + dpp<kRowRor8>(v[0]);
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < H; ++m) {
+            const float a = v[m], b = H + m < N ? v[H + m] : v[m];
+            if constexpr (BIT == 3) {
+                // Within a DPP row (partner lane ^ 8): keep one, send the other.
+                w[m] = (hi ? b : a) + dpp<kRowRor8>(hi ? a : b);
+            } else {
+                // The swap leaves (a, partner's a) on the low lanes and
+                // (partner's b, b) on the high lanes: one add completes either.
+                const auto x = BIT == 5
+                                   ? __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false)
+                                   : __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+                w[m] = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+            }
+        }
+    }
+}
+
+template <int NC>
+__device__ __forceinline__ void scatter(const float (&x)[NC], float (&out)[Scatter<NC>::S], int q) {
+    using SC = Scatter<NC>;
+    float x1[SC::N1], x2[SC::N2];
+    scatter_step<5, NC>(x, x1, (q & 4) != 0);
+    scatter_step<4, SC::N1>(x1, x2, (q & 2) != 0);
+    scatter_step<3, SC::N2>(x2, out, (q & 1) != 0);
+}
+
+// out = K w for the column-layout w, in the slot layout (NR row blocks).
+template <int NR, int NC>
+__device__ __forceinline__ void kmul(const float (&K)[NR][NC], const float (&wc)[NC], float (&out)[Scatter<NR>::S],
+                                     int q) {
+    float x[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) x[r] = K[r][0] * wc[0];
+#pragma unroll
+    for (int t = 1; t < NC; ++t)
+#pragma unroll
+        for (int r = 0; r < NR; ++r) x[r] = __builtin_fmaf(K[r][t], wc[t], x[r]);
+    scatter<NR>(x, out, q);
+}
+
+// Buffer descriptor over the cost from row 8r on (reads past the end of the
+// cost return 0); one per row block, so that a lane's byte offset into it is
+// the same register for every block and the column block an immediate.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t block_rsrc(const float *C, int d, int r) {
+    const int rest = d * d - 8 * r * d;
+    return __builtin_amdgcn_make_buffer_rsrc((void *)(C + (size_t)8 * r * d), (short)0, rest > 0 ? 4 * rest : 0,
+                                             0x00020000);
+}
+__device__ __forceinline__ float load_cell(__amdgpu_buffer_rsrc_t rsrc, int byte_off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, byte_off, 0, 0));
+}
+
+// Work-group = one problem, two wavefronts: wavefront w holds the row blocks
+// r in [w H, w H + H), H = ceil(NC / 2), against every column block, so each
+// computes whole row sums of its rows; the updated scalings meet in LDS (one
+// barrier per product).  Two wavefronts per problem put two per SIMD for a
+// batch of one problem per SIMD: a single wavefront issues a vector
+// instruction only every few cycles, two interleave.
+template <int NC>
+__global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
+    constexpr int H = (NC + 1) / 2;
+    constexpr int S = Scatter<H>::S;
+    static_assert(S == 1, "one slot per lane");
+    // Column operand in LDS, by column block: row y at [y & 7][y >> 3], so
+    // that lane (p, q) reads its NC values contiguously (16-byte reads; a
+    // stride of 20 floats puts the 8 blocks q on distinct banks).
+    constexpr int XS = 20;
+    static_assert(2 * H <= XS, "row blocks per column-block line");
+    __shared__ __attribute__((aligned(16))) float xs[2][8 * XS];  // xs[0] = U, xs[1] = V
+    // Per-wavefront reports: [iteration parity][phase][wavefront][error, failure].
+    // The parity keeps a report readable until both wavefronts have passed
+    // the next iteration's barriers.
+    __shared__ float red[2][2][2][2];
+    __shared__ float ini[2][2][4];  // set-up exchanges
+
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: descriptors stay scalar
+    const int p = lane & 7, q = lane >> 3;
+    const int b = blockIdx.x;
+    const int d = A.d1;
+    const float s = A.s;
+    const int r0 = w * H;  // first row block of this wavefront
+
+    // Raw cost cells of the wavefront's row blocks, and the transposed cells
+    // (q + 8t, p + 8r) for the symmetry check: rows past d read 0, columns
+    // past d the next row's cells; every such cell is masked.
+    const int voff = (p * d + q) * 4, toff = (q * d + p) * 4;
+    const int rlim = (d - p + 7) >> 3, tlim = (d - q + 7) >> 3;
+    float K[H][NC];
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+        const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, r0 + i);
+#pragma unroll
+        for (int t = 0; t < NC; ++t) K[i][t] = load_cell(rs, voff + 32 * t);
+    }
+    bool asym = false;
+#pragma unroll
+    for (int t = 0; t < NC; ++t) {
+        const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, t);
+        bool ne = false;
+#pragma unroll
+        for (int i = 0; i < H; ++i)
+            ne |= (r0 + i < rlim) & (__float_as_uint(load_cell(rs, toff + 32 * (r0 + i))) != __float_as_uint(K[i][t]));
+        asym |= (t < tlim) & ne;
+    }
+    float mx = neg_inf(), mn = __builtin_inff();
+    bool nan = false;
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+        float rmx = neg_inf(), rmn = __builtin_inff();
+        bool rnan = false;
+#pragma unroll
+        for (int t = 0; t < NC; ++t) {
+            const bool in = t < tlim;
+            rmx = fmaxf(rmx, in ? K[i][t] : neg_inf());
+            rmn = fminf(rmn, in ? K[i][t] : __builtin_inff());
+            rnan |= in & (K[i][t] != K[i][t]);
+        }
+        const bool in = r0 + i < rlim;
+        mx = fmaxf(mx, in ? rmx : neg_inf());
+        mn = fminf(mn, in ? rmn : __builtin_inff());
+        nan |= in & rnan;
+    }
+    // (Wavefront-wide votes and reductions are taken by every lane, before
+    // lane 0 publishes them.)
+    mx = wave_max(mx);
+    mn = -wave_max(-mn);
+    const float fasym = __any(asym) ? 1.f : 0.f, fnan = __any(nan) ? 1.f : 0.f;
+    if (lane == 0) {
+        ini[0][w][0] = fasym;
+        ini[0][w][1] = fnan;
+        ini[0][w][2] = mn;
+        ini[0][w][3] = mx;
+    }
+    __syncthreads();
+    if (ini[0][0][0] + ini[0][1][0] != 0.f) {  // the same verdict for every problem: the cost is shared
+        if (threadIdx.x == 0) A.iters[b] = -2;
+        return;
+    }
+    // Raw cost range -> cl range (cl = -s C with s > 0: the extremes swap).
+    const float clmax = -s * fminf(ini[0][0][2], ini[0][1][2]);
+    const float clmin = -s * fmaxf(ini[0][0][3], ini[0][1][3]);
+    if (ini[0][0][1] + ini[0][1][1] != 0.f || !(clmax - clmin <= kRangeBits)) {  // a non-finite cost fails too
+        if (threadIdx.x == 0) A.iters[b] = -1;
+        return;
+    }
+    // K on the cells of the problem; elsewhere a finite value in (0, 1]
+    // (the clamp), which meets only zero operands and unused rows.
+#pragma unroll
+    for (int i = 0; i < H; ++i)
+#pragma unroll
+        for (int t = 0; t < NC; ++t) K[i][t] = ex2(fminf(-s * K[i][t] - clmax, 0.f));
+
+    // The lane's slot: row x = p + 8 (r0 + rr) of its wavefront, or none
+    // (own = false: a duplicate after an all-reduce step).  Marginals are 0
+    // off the problem.
+    int rr = -1;
+#pragma unroll
+    for (int qq = 0; qq < 8; ++qq)
+        if (q == qq) rr = scatter_row(H, qq, 0);
+    const bool own = rr >= 0;
+    const int x = own ? p + 8 * (r0 + rr) : 0;
+    const int xl = p * XS + r0 + rr;  // its place in the LDS operand
+    const float ms = own && x < d ? A.mu[(size_t)b * d + x] : 0.f;
+    const float ns = own && x < d ? A.nu[(size_t)b * d + x] : 0.f;
+    {
+        const float cm = wave_sum(ms > 0.f ? 1.f : 0.f), cn = wave_sum(ns > 0.f ? 1.f : 0.f);
+        if (lane == 0) {
+            ini[1][w][0] = cm;
+            ini[1][w][1] = cn;
+        }
+    }
+    // Column operand of the first product: u^0 = 1 on the support of mu.
+    if (own) xs[0][xl] = ms > 0.f ? 1.f : 0.f;
+    __syncthreads();
+    if (ini[1][0][0] + ini[1][1][0] == 0.f || ini[1][0][1] + ini[1][1][1] == 0.f) {  // empty support
+        if (threadIdx.x == 0) A.iters[b] = -1;
+        return;
+    }
+
+    const int n_iter = A.n_iter;
+    const float tol = A.tol;
+    const bool check = tol > 0.f;
+    int kstop = n_iter;
+    float U = 0.f, V, Vold = 0.f, X[S], wc[NC];
+
+    // Column layout from LDS: register t of lane (p, q) takes row q + 8t.
+    auto gather_lds = [&](const float *src) {
+        const float *line = src + q * XS;
+#pragma unroll
+        for (int t = 0; t + 4 <= NC; t += 4) {
+            const float4 v4 = *reinterpret_cast<const float4 *>(line + t);
+            wc[t] = v4.x;
+            wc[t + 1] = v4.y;
+            wc[t + 2] = v4.z;
+            wc[t + 3] = v4.w;
+        }
+#pragma unroll
+        for (int t = NC & ~3; t < NC; ++t) wc[t] = line[t];
+    };
+    // v-update of iteration 1.
+    gather_lds(xs[0]);
+    kmul<H, NC>(K, wc, X, q);
+    {
+        const float v = ns * __builtin_amdgcn_rcpf(X[0]);
+        const bool bad = (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+        V = ns > 0.f ? v : 0.f;
+        if (own) xs[1][xl] = V;
+        const float fb = __any(bad) ? 1.f : 0.f;
+        if (lane == 0) red[0][1][w][1] = fb;
+    }
+    __syncthreads();
+    bool fail = red[0][1][0][1] + red[0][1][1][1] != 0.f;
+
+    // Iteration k: R = K V and the u-update; then (k < n_iter) S = K^T U = K U,
+    // the stop test of iterate k (its row error from the u-update, its column
+    // error from S and the V it was built with) and the v-update of k+1.
+    for (int k = 1; !fail && k <= n_iter; ++k) {
+        float(&rd)[2][2][2] = red[k & 1];
+        gather_lds(xs[1]);
+        kmul<H, NC>(K, wc, X, q);
+        {
+            const float u = ms * __builtin_amdgcn_rcpf(X[0]);
+            const bool bad = (ms > 0.f) & !(sum_ok(X[0]) & scale_ok(u));
+            U = ms > 0.f ? u : 0.f;
+            if (own) xs[0][xl] = U;
+            const float e = check ? wave_sum(ms > 0.f ? fabsf(u * X[0] - ms) : 0.f) : 0.f;
+            const float fb = __any(bad) ? 1.f : 0.f;
+            if (lane == 0) {
+                rd[0][w][0] = e;
+                rd[0][w][1] = fb;
+            }
+        }
+        __syncthreads();
+        if (k == n_iter) {
+            fail = rd[0][0][1] + rd[0][1][1] != 0.f;
+            break;
+        }
+
+        // (A failed u-update is acted on after the next barrier: the product
+        // in between only spends time.)
+        gather_lds(xs[0]);
+        kmul<H, NC>(K, wc, X, q);
+        {
+            const float e = check ? wave_sum(ns > 0.f ? fabsf(V * X[0] - ns) : 0.f) : 0.f;
+            const float v = ns * __builtin_amdgcn_rcpf(X[0]);
+            const bool bad = (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+            Vold = V;
+            V = ns > 0.f ? v : 0.f;
+            if (own) xs[1][xl] = V;
+            const float fb = __any(bad) ? 1.f : 0.f;
+            if (lane == 0) {
+                rd[1][w][0] = e;
+                rd[1][w][1] = fb;
+            }
+        }
+        __syncthreads();
+        if (rd[0][0][1] + rd[0][1][1] != 0.f) {  // the u-update of iterate k failed
+            fail = true;
+            break;
+        }
+        if (check && (rd[0][0][0] + rd[0][1][0]) + (rd[1][0][0] + rd[1][1][0]) <= tol) {
+            kstop = k;  // the returned plan is iterate k: U and the V it was built with
+            V = Vold;
+            break;
+        }
+        fail = rd[1][0][1] + rd[1][1][1] != 0.f;
+    }
+    if (fail) {
+        if (threadIdx.x == 0) A.iters[b] = -1;
+        return;
+    }
+
+    // ---- the returned plan P = U K V, measured (Section 4): its marginals
+    // and sum_ij P_ij C_ij from the cost itself.  No wavefront reads the
+    // operand buffers between the loop's last barrier and here. ----
+    if (own) xs[1][xl] = V;
+    __syncthreads();
+    gather_lds(xs[1]);
+    kmul<H, NC>(K, wc, X, q);  // row sums R = K V
+    float err = ms > 0.f ? fabsf(U * X[0] - ms) : 0.f, lsum;
+    {
+        // L_i = sum_j K_ij V_j C_ij with the cells reloaded (K is 0 off the
+        // problem, where the loaded cost is 0 or a finite neighbour).
+        float l[H], ls[S];
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+            const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, r0 + i);
+            float acc = 0.f;
+#pragma unroll
+            for (int t = 0; t < NC; ++t) acc = __builtin_fmaf(K[i][t] * wc[t], load_cell(rs, voff + 32 * t), acc);
+            l[i] = acc;
+        }
+        scatter<H>(l, ls, q);
+        lsum = ms > 0.f ? U * ls[0] : 0.f;
+    }
+    gather_lds(xs[0]);
+    kmul<H, NC>(K, wc, X, q);  // column sums S = K^T U
+    err += ns > 0.f ? fabsf(V * X[0] - ns) : 0.f;
+    err = wave_sum(err);
+    lsum = wave_sum(lsum);
+    if (lane == 0) {
+        red[0][0][w][0] = err;
+        red[0][0][w][1] = lsum;
+    }
+    if (own && x < d) {
+        A.alpha[(size_t)b * d + x] = kLn2 * lg2(U);
+        A.beta[(size_t)b * d + x] = kLn2 * (lg2(V) - clmax);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        A.loss[b] = red[0][0][0][1] + red[0][0][1][1];
+        A.marg_err[b] = red[0][0][0][0] + red[0][0][1][0];
+        A.iters[b] = kstop;
+    }
+}
+
+template <int NC>
+hipError_t launch_nc(const FwdArgs &a, hipStream_t st) {
+    hipLaunchKernelGGL((sk_resident_sym_kernel<NC>), dim3(a.B), dim3(128), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool launch_resident_sym(const FwdArgs &a, hipStream_t st, hipError_t *err) {
+    if (a.n_iter <= 0 || a.c_batched || a.d1 != a.d2) return false;
+    const int nc = (a.d1 + 7) / 8;
+    if (nc <= 2) *err = launch_nc<2>(a, st);
+    else if (nc <= 4) *err = launch_nc<4>(a, st);
+    else if (nc <= 8) *err = launch_nc<8>(a, st);
+    else if (nc <= 13) *err = launch_nc<13>(a, st);
+    else return false;
+    return true;
+}
+
+}  // namespace sk

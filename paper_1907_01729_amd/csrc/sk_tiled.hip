@@ -1128,6 +1128,14 @@ template <int NCW, int W, bool VEC4>
 hipError_t run_shared(const TiledArgs &T, hipStream_t st) {
     constexpr int RS = SharedShape<NCW>::RS, RB = SharedShape<NCW>::RB;
     const size_t lds = sizeof(float) * 2 * RS * NCW * 64;
+    static bool attr = false;  // chunk buffers above 64 KB need the larger dynamic LDS limit
+    if (!attr) {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        attr = true;
+    }
     const dim3 grid(T.R, (T.B + W - 1) / W), blk(64 * W);
     return run_sequence(
         T, st,

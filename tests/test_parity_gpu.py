@@ -92,10 +92,11 @@ def check_backward(prob, gpu, ref, idx=None, grad_C=False, seed=0):
         assert e3 <= GRAD_RTOL
 
 
-@pytest.fixture(params=["auto", "log"])
+@pytest.fixture(params=["auto", "nosym", "log"])
 def form(request, monkeypatch):
-    """Resident regime: the plain-form kernel with its log-domain fallback
-    (the default), or the log-domain kernel alone."""
+    """Resident regime: the plain-form kernels with their fallbacks (the
+    default), the same without the symmetric-cost kernel (symmetric costs go
+    to the matrix-core kernel), or the log-domain kernel alone."""
     monkeypatch.setenv("SK_RESIDENT_FORM", request.param)
     return request.param
 
@@ -263,6 +264,61 @@ def test_plain_early_stop_agrees_with_log(monkeypatch):
         monkeypatch.setenv("SK_RESIDENT_FORM", f)
         out[f] = check_forward(prob)[0]
     assert np.all(out["plain"]["iters"] >= 0)
+    assert np.all(np.abs(out["plain"]["iters"] - out["log"]["iters"]) <= 1)
+
+
+# ---------------------------------------------------------------- symmetric shared cost, one wavefront per problem
+
+@pytest.mark.parametrize("d", [1, 2, 7, 8, 9, 16, 17, 33, 64, 65, 100, 104])
+def test_sym_kernel_shapes(d, monkeypatch):
+    """Every register-tile width of the symmetric-cost kernel, ragged tails
+    included; alone (plain) it solves every problem."""
+    prob = workloads.random_problem(seed=300 + d, B=5, d1=d, d2=d, lam=0.1, n_iter=60, cost="sym")
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_sym_kernel_zero_masses(monkeypatch):
+    prob = workloads.random_problem(seed=31, B=7, d1=90, d2=90, lam=0.05, n_iter=120, cost="sym", zero_frac=0.3)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_sym_kernel_hands_over_asymmetric_cost(monkeypatch):
+    """An asymmetric cost (one pair differs) is handed to the matrix-core
+    kernel: iters = -2 from the symmetric kernel alone, and with the fallback
+    the same bits as the path without the symmetric kernel."""
+    prob = workloads.random_problem(seed=32, B=6, d1=50, d2=50, lam=0.1, n_iter=50, cost="sym")
+    prob.C[0, 3, 41] += 0.25
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    assert np.all(_gpu(prob)["iters"] == -2)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "nosym")
+    ref_bits = _gpu(prob)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    gpu, ref = check_forward(prob)
+    for k in ("alpha", "beta", "loss", "marg_err", "iters"):
+        np.testing.assert_array_equal(gpu[k], ref_bits[k])
+
+
+def test_sym_kernel_hands_over_out_of_range(monkeypatch):
+    """lambda = 1e-3 on a symmetric 1-D grid cost (spread > 1000 bits): iters
+    = -1 from the symmetric kernel alone; the log-domain kernel solves it."""
+    prob = workloads.random_problem(seed=33, B=3, d1=60, d2=60, lam=1e-3, n_iter=100, cost="grid1d")
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    assert np.all(_gpu(prob)["iters"] == -1)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    check_forward(prob, merr_atol=1e-4)
+
+
+def test_sym_kernel_early_stop(monkeypatch):
+    prob = workloads.random_problem(seed=34, B=8, d1=80, d2=80, lam=0.1, n_iter=400, tol=1e-5, cost="sym")
+    out = {}
+    for f in ("plain", "log"):
+        monkeypatch.setenv("SK_RESIDENT_FORM", f)
+        out[f] = check_forward(prob)[0]
+    assert np.all(out["plain"]["iters"] >= 1) and np.all(out["plain"]["iters"] < 400)
     assert np.all(np.abs(out["plain"]["iters"] - out["log"]["iters"]) <= 1)
 
 

@@ -164,7 +164,8 @@ def random_problem(seed, B, d1, d2, lam, n_iter, c_batched=False, zero_frac=0.0,
                    cost="uniform", tol=0.0):
     """Generic random problem for edge cases: positive histograms (optionally
     with a fraction of exact zeros, at least one non-zero kept per sample) and
-    a non-symmetric cost U[0,1) (or 'grid1d': |x_i - y_j| on [0,1])."""
+    a non-symmetric cost U[0,1) (or 'grid1d': |x_i - y_j| on [0,1]; or 'sym':
+    (U + U^T) / 2 for d1 = d2, exactly symmetric)."""
     rng = np.random.default_rng(seed)
     mu = rng.uniform(0.05, 1.0, size=(B, d1))
     nu = rng.uniform(0.05, 1.0, size=(B, d2))
@@ -177,6 +178,10 @@ def random_problem(seed, B, d1, d2, lam, n_iter, c_batched=False, zero_frac=0.0,
     nC = B if c_batched else 1
     if cost == "uniform":
         C = rng.uniform(0.0, 1.0, size=(nC, d1, d2))
+    elif cost == "sym":
+        assert d1 == d2, "a symmetric cost needs d1 == d2"
+        U = rng.uniform(0.0, 1.0, size=(nC, d1, d2))
+        C = 0.5 * (U + np.swapaxes(U, 1, 2))
     elif cost == "grid1d":
         x = np.linspace(0.0, 1.0, d1)
         y = np.linspace(0.0, 1.0, d2)
