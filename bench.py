@@ -63,6 +63,8 @@ WORKLOAD_NAMES = {
        "500 iterations, tol=1e-6 + backward",
     5: "clouds: B=32, d1=1024, d2=2048, per-sample squared-distance cost [32,1024,2048], lambda=0.05, "
        "100 iterations + backward with grad_C",
+    6: "clouds from points: the clouds workload with the cost recreated from the 3-D coordinates in the sweep "
+       "(no cost matrix), B=32, d1=1024, d2=2048, lambda=0.05, 100 iterations + backward with grad_X, grad_Y",
 }
 
 
@@ -116,12 +118,31 @@ def cpu_baseline_sampled(prob, grad_C, n_samples):
     return r
 
 
+def cpu_baseline_points(prob, n_samples):
+    """The oracle on the first problems of a point-cloud workload: the cost from
+    the coordinates, forward, backward and the point gradients."""
+    import oracle
+
+    idx = np.arange(n_samples)
+    t0 = time.perf_counter()
+    C = oracle.cost_from_points(prob.X[idx], prob.Y[idx])
+    o = oracle.forward(prob.mu[idx], prob.nu[idx], C, prob.lam, prob.n_iter, tol=prob.tol)
+    r = oracle.backward(np.ones(n_samples), prob.mu[idx], prob.nu[idx], C, prob.lam, o["alpha"], o["beta"],
+                        grad_C=True)
+    oracle.points_grads(r["grad_C"], prob.X[idx], prob.Y[idx])
+    dt = time.perf_counter() - t0
+    cells = float(np.sum(o["iters"].astype(np.float64))) * prob.d1 * prob.d2
+    return dict(value=cells / dt, unit="cell-updates/s", cores=oracle.num_threads(), kind="oracle",
+                sample=f"first {n_samples} of {prob.B} problems of workload {prob.name}, cost from the points, "
+                       f"one forward+backward with point gradients, {dt:.2f} s")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 3 times (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -146,19 +167,41 @@ def main():
     import paper_1907_01729_amd as sk
     import workloads
 
-    prob = workloads.make_config(args.config)
-    grad_C = bool(prob.grad_C)
+    points = args.config == 6
+    prob = workloads.clouds_points() if points else workloads.make_config(args.config)
+    grad_C = bool(prob.grad_points) if points else bool(prob.grad_C)
     dev = torch.device("cuda:0")
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
-    mu, nu, C = t(prob.mu), t(prob.nu), t(prob.C)
+    mu, nu = t(prob.mu), t(prob.nu)
     g = torch.ones(prob.B, device=dev, dtype=torch.float32)
-    ws = torch.empty((max(sk.sinkhorn_workspace_bytes(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.lam,
-                                                      prob.n_iter, prob.tol), 1),), device=dev, dtype=torch.uint8)
+    if points:
+        X, Y = t(prob.X), t(prob.Y)
+        nws = sk.sinkhorn_points_workspace_bytes(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.D, prob.lam,
+                                                 prob.n_iter, prob.tol)
+        ws = torch.empty((max(nws, 1),), device=dev, dtype=torch.uint8)
+
+        def fwd(n):
+            return sk.sinkhorn_forward_points(mu, nu, X, Y, prob.lam, n, prob.tol, workspace=ws)
+
+        def bwd(out):
+            return sk.sinkhorn_backward_points(g, mu, nu, X, Y, prob.lam, out["alpha"], out["beta"],
+                                               grad_points=grad_C)
+    else:
+        C = t(prob.C)
+        nws = sk.sinkhorn_workspace_bytes(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.lam, prob.n_iter,
+                                          prob.tol)
+        ws = torch.empty((max(nws, 1),), device=dev, dtype=torch.uint8)
+
+        def fwd(n):
+            return sk.sinkhorn_forward(mu, nu, C, prob.lam, n, prob.tol, workspace=ws)
+
+        def bwd(out):
+            return sk.sinkhorn_backward(g, mu, nu, C, prob.lam, out["alpha"], out["beta"], grad_C=grad_C)
     regime = sk.sinkhorn_regime(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.lam, prob.n_iter, prob.tol)
 
     def step():
-        out = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter, prob.tol, workspace=ws)
-        sk.sinkhorn_backward(g, mu, nu, C, prob.lam, out["alpha"], out["beta"], grad_C=grad_C)
+        out = fwd(prob.n_iter)
+        bwd(out)
         return out
 
     for _ in range(args.warmup):
@@ -175,9 +218,9 @@ def main():
     e_all0.record(stream)
     for k in range(args.steps):
         ev[k][0].record(stream)
-        out = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter, prob.tol, workspace=ws)
+        out = fwd(prob.n_iter)
         ev[k][1].record(stream)
-        sk.sinkhorn_backward(g, mu, nu, C, prob.lam, out["alpha"], out["beta"], grad_C=grad_C)
+        bwd(out)
     e_all1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -197,7 +240,7 @@ def main():
         kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
         for k in range(args.steps):
             kev[k][0].record(stream)
-            kout = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter, prob.tol, workspace=ws)
+            kout = fwd(prob.n_iter)
             kev[k][1].record(stream)
         torch.cuda.synchronize()
         del os.environ["SK_RESIDENT_FORM"]
@@ -219,22 +262,31 @@ def main():
         # fixed launches exactly.  Shared cost: exp bound, one exp2 per cell
         # per sweep.  Per-sample cost: HBM bound, the cost read once per sweep.
         n_hi, n_lo = prob.n_iter, max(prob.n_iter // 2, 1)
-        fwd = {}
+        tfwd = {}
         for n in (n_lo, n_hi):
-            sk.sinkhorn_forward(mu, nu, C, prob.lam, n, prob.tol, workspace=ws)
+            fwd(n)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             reps = max(2, args.steps // 2)
             e0.record(stream)
             for _ in range(reps):
-                o = sk.sinkhorn_forward(mu, nu, C, prob.lam, n, prob.tol, workspace=ws)
+                o = fwd(n)
             e1.record(stream)
             torch.cuda.synchronize()
-            fwd[n] = (e0.elapsed_time(e1) / reps, float(o["iters"].cpu().numpy().astype(np.float64).sum()))
-        sweeps = (fwd[n_hi][1] - fwd[n_lo][1]) / prob.B  # sweeps per problem between the two runs
-        kernel_ms = (fwd[n_hi][0] - fwd[n_lo][0]) / max(sweeps, 1.0)
+            tfwd[n] = (e0.elapsed_time(e1) / reps, float(o["iters"].cpu().numpy().astype(np.float64).sum()))
+        sweeps = (tfwd[n_hi][1] - tfwd[n_lo][1]) / prob.B  # sweeps per problem between the two runs
+        kernel_ms = (tfwd[n_hi][0] - tfwd[n_lo][0]) / max(sweeps, 1.0)
         cells = float(prob.B) * prob.d1 * prob.d2
         src = kernel_source_hash(["sk_tiled.hip", "sk_device.h"])
-        if prob.c_batched:
+        if points:
+            # The cost is recreated from the coordinates: nothing streams, the
+            # sweep is bound by one exp2 per cell (plus the distance arithmetic);
+            # timed with its merge, like the shared-cost sweep.
+            kname = "sk_tiled_sweep_points"
+            achieved = cells / (kernel_ms * 1e-3) / 1e12
+            roof = dict(bound="alu", achieved=round(achieved, 4), peak=round(PEAK_EXP_TS, 4), unit="Texp/s",
+                        frac=round(achieved / PEAK_EXP_TS, 4), kernel=kname + " + sk_tiled_merge",
+                        kernel_ms=round(kernel_ms, 5), work="exp2 per iteration = B*d1*d2 (one per cell)")
+        elif prob.c_batched:
             kname = "sk_tiled_sweep_stream"
             nbytes = 4.0 * cells
             achieved = nbytes / (kernel_ms * 1e-3) / 1e9
@@ -270,12 +322,15 @@ def main():
             "workload": WORKLOAD_NAMES[args.config],
             "B": prob.B, "d1": prob.d1, "d2": prob.d2, "lambda": prob.lam, "n_iter": prob.n_iter,
             "tol": prob.tol, "c_batched": bool(prob.c_batched), "iters_done_mean": float(iters.mean()),
+            **({"D": prob.D, "cost": "from points"} if points else {}),
             "regime": {1: "resident", 2: "tiled"}.get(regime, "?"),
         },
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        if args.config in (1, 2):
+        if points:
+            res["cpu_baseline"] = cpu_baseline_points(prob, 2)
+        elif args.config in (1, 2):
             res["cpu_baseline"] = cpu_baseline(prob, grad_C)
         else:
             res["cpu_baseline"] = cpu_baseline_sampled(prob, grad_C, {3: 16, 4: 1, 5: 2}[args.config])

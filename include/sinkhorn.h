@@ -86,14 +86,17 @@ SK_API size_t sinkhorn_workspace_bytes(const sk_problem *p);
  *
  * For max(d1, d2) <= 128 the same iterates are first computed in the plain
  * form of eq. (sk_plain), u = mu / (K v), v = nu / (K^T u), with K scaled by
- * its largest entry (on the matrix cores when C is shared); a problem whose
- * scaled cost spans more than 64 bits, or whose sums or scalings leave a
- * guarded fp32 range at any iteration, is re-solved from the start by the
- * log-domain kernel launched right after it on the same stream.  Diagnostic
- * switch (environment variable SK_RESIDENT_FORM, read at every call): "log"
- * runs the log-domain kernel only; "plain" runs the plain form only, leaving
- * the problems it cannot keep in range with iters = -1 and their other
- * outputs unspecified.
+ * its largest entry (a shared symmetric C with d1 = d2 <= 104: on the vector
+ * ALU, K^T u = K u; another shared C: on the matrix cores; a per-sample C: on
+ * the vector ALU); a problem whose scaled cost spans more than 64 bits, or
+ * whose sums or scalings leave a guarded fp32 range at any iteration, is
+ * re-solved from the start by the log-domain kernel launched right after it
+ * on the same stream.  Diagnostic switch (environment variable
+ * SK_RESIDENT_FORM, read at every call): "log" runs the log-domain kernel
+ * only; "plain" runs the first-choice plain-form kernel only, leaving the
+ * problems it hands over with iters = -1 (out of range) or -2 (cost not
+ * symmetric) and their other outputs unspecified; "nosym" skips the
+ * symmetric-cost kernel.
  *
  *   mu        [B, d1]              input histograms
  *   nu        [B, d2]
@@ -133,6 +136,45 @@ SK_API sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss,
                             const float *alpha, const float *beta,
                             float *grad_mu, float *grad_nu, float *grad_C,
                             void *stream);
+
+/*
+ * Point clouds.  The cost is the squared Euclidean distance between points,
+ *     C_ij = sum_k (X[i,k] - Y[j,k])^2,   k < D,   1 <= D <= 16,
+ * with X [d1, D] and Y [d2, D] shared by the batch (c_batched = 0) or
+ * X [B, d1, D] and Y [B, d2, D] per sample (c_batched = 1).  Everything else
+ * is as in sinkhorn_forward / sinkhorn_backward with that C.  Section 4 notes
+ * that cost entries can be recreated from the points rather than stored: for
+ * per-sample clouds with max(d1, d2) > 128, d2 <= 2048 and D <= 3 the tiled
+ * sweep does exactly that and no cost matrix exists (the cost is
+ * -|r x_i - r y_j|^2 in the scaled base-2 units, r = sqrt(log2(e)/lambda),
+ * evaluated in fp32); every other shape writes C into the workspace first and
+ * runs the forward above on it.
+ *
+ * Bytes of workspace sinkhorn_forward_points needs (0 for an invalid problem
+ * or D).
+ */
+SK_API size_t sinkhorn_points_workspace_bytes(const sk_problem *p, int32_t D);
+
+SK_API sk_status sinkhorn_forward_points(const sk_problem *p, int32_t D, const float *mu,
+                                  const float *nu, const float *X, const float *Y,
+                                  float *alpha, float *beta, float *loss, float *marg_err,
+                                  int32_t *iters, void *workspace, size_t ws_bytes,
+                                  void *stream);
+
+/*
+ * Backward for point clouds: grad_mu and grad_nu as in sinkhorn_backward, and
+ * (optional, either may be NULL) the gradient with respect to the points by
+ * the chain rule through dW/dC = P:
+ *   grad_X[b,i,:] = g_b * sum_j P_b,ij * 2 (X[b,i,:] - Y[b,j,:]),
+ *   grad_Y[b,j,:] = g_b * sum_i P_b,ij * 2 (Y[b,j,:] - X[b,i,:]),
+ * summed over the batch for shared clouds (shapes as X and Y).  P is rebuilt
+ * from alpha, beta and the points; needs no workspace; deterministic.
+ */
+SK_API sk_status sinkhorn_backward_points(const sk_problem *p, int32_t D, const float *grad_loss,
+                                   const float *mu, const float *nu, const float *X,
+                                   const float *Y, const float *alpha, const float *beta,
+                                   float *grad_mu, float *grad_nu, float *grad_X,
+                                   float *grad_Y, void *stream);
 
 /* Static description of a status code (never NULL). */
 SK_API const char *sinkhorn_status_string(sk_status s);

@@ -152,3 +152,40 @@ def plan(C, lam, alpha, beta):
     if rc != 0:
         raise ValueError("oracle_plan: invalid arguments")
     return P
+
+
+# ---- point clouds ----
+
+def cost_from_points(X, Y):
+    """Squared Euclidean cost by its definition, C_ij = sum_k (X_ik - Y_jk)^2,
+    in fp64 (differences first, no expansion).  X [nb, d1, D] or [d1, D],
+    Y [nb, d2, D] or [d2, D]  ->  C [nb, d1, d2]."""
+    X, Y = _f64(X), _f64(Y)
+    if X.ndim == 2:
+        X = X[None]
+    if Y.ndim == 2:
+        Y = Y[None]
+    C = np.empty((X.shape[0], X.shape[1], Y.shape[1]))
+    for b in range(X.shape[0]):  # one cloud pair at a time: bounded memory
+        diff = X[b][:, None, :] - Y[b][None, :, :]
+        C[b] = (diff * diff).sum(-1)
+    return C
+
+
+def points_grads(G, X, Y):
+    """Chain rule through C_ij = |X_i - Y_j|^2 for a cost gradient G = dW/dC
+    [nb, d1, d2]: grad_X_i = sum_j G_ij 2 (X_i - Y_j), grad_Y_j = sum_i G_ij
+    2 (Y_j - X_i), per cloud pair, in fp64."""
+    X, Y, G = _f64(X), _f64(Y), _f64(G)
+    if X.ndim == 2:
+        X = X[None]
+    if Y.ndim == 2:
+        Y = Y[None]
+    if G.ndim == 2:
+        G = G[None]
+    gX = np.empty_like(X)
+    gY = np.empty_like(Y)
+    for b in range(X.shape[0]):
+        gX[b] = 2.0 * (G[b].sum(1)[:, None] * X[b] - G[b] @ Y[b])
+        gY[b] = 2.0 * (G[b].sum(0)[:, None] * Y[b] - G[b].T @ X[b])
+    return gX, gY

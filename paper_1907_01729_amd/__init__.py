@@ -14,21 +14,29 @@ from ._binding import (  # noqa: F401
     library_path,
     load_library,
     sinkhorn_backward,
+    sinkhorn_backward_points,
     sinkhorn_forward,
+    sinkhorn_forward_points,
+    sinkhorn_points_workspace_bytes,
     sinkhorn_regime,
     sinkhorn_status_string,
     sinkhorn_workspace_bytes,
 )
-from .loss import SinkhornLoss, sinkhorn_loss  # noqa: F401
+from .loss import SinkhornLoss, SinkhornPointsLoss, sinkhorn_loss, sinkhorn_loss_points  # noqa: F401
 
 __all__ = [
     "SinkhornError",
     "SinkhornLoss",
+    "SinkhornPointsLoss",
     "library_path",
     "load_library",
     "sinkhorn_backward",
+    "sinkhorn_backward_points",
     "sinkhorn_forward",
+    "sinkhorn_forward_points",
     "sinkhorn_loss",
+    "sinkhorn_loss_points",
+    "sinkhorn_points_workspace_bytes",
     "sinkhorn_regime",
     "sinkhorn_status_string",
     "sinkhorn_workspace_bytes",

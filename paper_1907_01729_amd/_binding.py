@@ -26,6 +26,9 @@ EXPORTED = (
     "sinkhorn_backward",
     "sinkhorn_status_string",
     "sinkhorn_regime",
+    "sinkhorn_points_workspace_bytes",
+    "sinkhorn_forward_points",
+    "sinkhorn_backward_points",
 )
 
 
@@ -73,6 +76,13 @@ def load_library():
     lib.sinkhorn_status_string.restype = ctypes.c_char_p
     lib.sinkhorn_regime.argtypes = [PP]
     lib.sinkhorn_regime.restype = ctypes.c_int32
+    I = ctypes.c_int32
+    lib.sinkhorn_points_workspace_bytes.argtypes = [PP, I]
+    lib.sinkhorn_points_workspace_bytes.restype = ctypes.c_size_t
+    lib.sinkhorn_forward_points.argtypes = [PP, I, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.sinkhorn_forward_points.restype = ctypes.c_int
+    lib.sinkhorn_backward_points.argtypes = [PP, I, P, P, P, P, P, P, P, P, P, P, P, P]
+    lib.sinkhorn_backward_points.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -174,4 +184,81 @@ def sinkhorn_backward(grad_loss, mu, nu, C, lam, alpha, beta, grad_C=False, stre
     out = dict(grad_mu=gmu, grad_nu=gnu)
     if grad_C:
         out["grad_C"] = gC
+    return out
+
+
+def _point_shapes(mu, nu, X, Y):
+    if mu.dim() != 2 or nu.dim() != 2 or mu.shape[0] != nu.shape[0]:
+        raise ValueError(f"mu must be [B,d1] and nu [B,d2], got {tuple(mu.shape)} {tuple(nu.shape)}")
+    B, d1 = mu.shape
+    d2 = nu.shape[1]
+    if X.dim() == 2:
+        X = X.unsqueeze(0)
+    if Y.dim() == 2:
+        Y = Y.unsqueeze(0)
+    if X.dim() != 3 or Y.dim() != 3 or X.shape[0] != Y.shape[0] or X.shape[2] != Y.shape[2]:
+        raise ValueError(f"X must be [(B,)d1,D] and Y [(B,)d2,D], got {tuple(X.shape)} {tuple(Y.shape)}")
+    if X.shape[1] != d1 or Y.shape[1] != d2 or X.shape[0] not in (1, B):
+        raise ValueError(f"X/Y shapes {tuple(X.shape)} {tuple(Y.shape)} do not match mu/nu")
+    c_batched = int(X.shape[0] == B and B != 1)
+    return B, d1, d2, c_batched, int(X.shape[2])
+
+
+def sinkhorn_points_workspace_bytes(B, d1, d2, c_batched, D, lam, n_iter, tol=0.0) -> int:
+    p = problem(B, d1, d2, c_batched, lam, n_iter, tol)
+    return int(load_library().sinkhorn_points_workspace_bytes(ctypes.byref(p), int(D)))
+
+
+def sinkhorn_forward_points(mu, nu, X, Y, lam, n_iter, tol=0.0, stream=None, workspace=None):
+    """Forward with the cost C_ij = |X_i - Y_j|^2 given by point clouds.
+
+    X [d1,D] | [1,d1,D] | [B,d1,D], Y [d2,D] | [1,d2,D] | [B,d2,D] (shared or per-sample clouds).
+    Returns the same dict as sinkhorn_forward.
+    """
+    lib = load_library()
+    for t, n in ((mu, "mu"), (nu, "nu"), (X, "X"), (Y, "Y")):
+        _dev(t, n)
+    B, d1, d2, cb, D = _point_shapes(mu, nu, X, Y)
+    p = problem(B, d1, d2, cb, lam, n_iter, tol)
+    dev = mu.device
+    f = dict(device=dev, dtype=torch.float32)
+    alpha = torch.empty((B, d1), **f)
+    beta = torch.empty((B, d2), **f)
+    loss = torch.empty((B,), **f)
+    merr = torch.empty((B,), **f)
+    iters = torch.empty((B,), device=dev, dtype=torch.int32)
+    need = int(lib.sinkhorn_points_workspace_bytes(ctypes.byref(p), D))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
+    st = lib.sinkhorn_forward_points(ctypes.byref(p), D, _ptr(mu), _ptr(nu), _ptr(X), _ptr(Y), _ptr(alpha),
+                                     _ptr(beta), _ptr(loss), _ptr(merr), _ptr(iters), _ptr(workspace),
+                                     ctypes.c_size_t(workspace.numel()), _stream(dev, stream))
+    if st != 0:
+        raise SinkhornError(st, "sinkhorn_forward_points")
+    return dict(alpha=alpha, beta=beta, loss=loss, marg_err=merr, iters=iters)
+
+
+def sinkhorn_backward_points(grad_loss, mu, nu, X, Y, lam, alpha, beta, grad_points=False, stream=None):
+    """Multiplier gradient for point clouds: dict(grad_mu, grad_nu[, grad_X, grad_Y])."""
+    lib = load_library()
+    for t, n in ((grad_loss, "grad_loss"), (mu, "mu"), (nu, "nu"), (X, "X"), (Y, "Y"), (alpha, "alpha"),
+                 (beta, "beta")):
+        _dev(t, n)
+    B, d1, d2, cb, D = _point_shapes(mu, nu, X, Y)
+    p = problem(B, d1, d2, cb, lam, 0, 0.0)
+    dev = mu.device
+    f = dict(device=dev, dtype=torch.float32)
+    gmu = torch.empty((B, d1), **f)
+    gnu = torch.empty((B, d2), **f)
+    gX = torch.empty(X.shape, **f) if grad_points else None
+    gY = torch.empty(Y.shape, **f) if grad_points else None
+    st = lib.sinkhorn_backward_points(ctypes.byref(p), D, _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(X), _ptr(Y),
+                                      _ptr(alpha), _ptr(beta), _ptr(gmu), _ptr(gnu), _ptr(gX), _ptr(gY),
+                                      _stream(dev, stream))
+    if st != 0:
+        raise SinkhornError(st, "sinkhorn_backward_points")
+    out = dict(grad_mu=gmu, grad_nu=gnu)
+    if grad_points:
+        out["grad_X"] = gX
+        out["grad_Y"] = gY
     return out

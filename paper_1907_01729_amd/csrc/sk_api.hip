@@ -39,6 +39,27 @@ int resident_form() {
     return kFormAuto;
 }
 
+sk::BwdArgs bwd_args(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu, const float *C,
+                     const float *alpha, const float *beta, float *grad_mu, float *grad_nu, float *grad_C) {
+    sk::BwdArgs a;
+    a.grad_loss = grad_loss;
+    a.mu = mu;
+    a.nu = nu;
+    a.C = C;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.grad_mu = grad_mu;
+    a.grad_nu = grad_nu;
+    a.grad_C = grad_C;
+    a.B = p->B;
+    a.d1 = p->d1;
+    a.d2 = p->d2;
+    a.c_batched = p->c_batched;
+    a.lambda = p->lambda;
+    a.s = sk::kLog2eHost / p->lambda;
+    return a;
+}
+
 // Resident regime.  First choice: the symmetric-cost kernel (shared cost,
 // d1 = d2 <= 104), else the matrix-core kernel (shared cost), else the
 // per-sample plain-form kernel.  Each hands over what it cannot solve: the
@@ -63,6 +84,60 @@ hipError_t launch_resident_regime(sk::FwdArgs a, int form, hipStream_t s) {
     return sk::launch_resident(a, s);
 }
 
+sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, const float *C, float *alpha,
+                     float *beta, float *loss, float *marg_err, int32_t *iters) {
+    sk::FwdArgs a;
+    a.mu = mu;
+    a.nu = nu;
+    a.C = C;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.loss = loss;
+    a.marg_err = marg_err;
+    a.iters = iters;
+    a.B = p->B;
+    a.d1 = p->d1;
+    a.d2 = p->d2;
+    a.n_iter = p->n_iter;
+    a.c_batched = p->c_batched;
+    a.lambda = p->lambda;
+    a.tol = p->tol;
+    a.s = sk::kLog2eHost / p->lambda;
+    a.only_flagged = 0;
+    return a;
+}
+
+// Regime dispatch of a forward over a cost matrix (tiled sweep, or the
+// resident kernels with their hand-overs).
+hipError_t run_forward(const sk::FwdArgs &a, void *workspace, hipStream_t s) {
+    if (!sk::resident_fits(a.d1, a.d2)) return sk::launch_tiled(a, workspace, s);
+    return launch_resident_regime(a, resident_form(), s);
+}
+
+// ---- point clouds ----
+
+constexpr int64_t kMaxPointFloats = int64_t(1) << 40;
+
+sk_status check_points(const sk_problem *p, int32_t D) {
+    const sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (D < 1 || D > sk::kPointsGradD) return SK_ERR_SHAPE;
+    const int64_t nb = p->c_batched ? p->B : 1;
+    if (nb * (int64_t)(p->d1 + (int64_t)p->d2) * D > kMaxPointFloats) return SK_ERR_SHAPE;
+    return SK_OK;
+}
+
+// Per-sample clouds of the tiled regime go through the on-the-fly sweep when
+// it takes the shape; everything else writes the cost out first.
+bool points_on_the_fly(const sk_problem *p, int32_t D) {
+    return p->c_batched && !sk::resident_fits(p->d1, p->d2) && sk::tiled_points_fits(p->B, p->d1, p->d2, D);
+}
+
+size_t cost_bytes(const sk_problem *p) {
+    const size_t n = sizeof(float) * (size_t)(p->c_batched ? p->B : 1) * p->d1 * p->d2;
+    return (n + 255) & ~size_t(255);
+}
+
 }  // namespace
 
 extern "C" {
@@ -85,6 +160,12 @@ int32_t sinkhorn_regime(const sk_problem *p) {
     return sk::resident_fits(p->d1, p->d2) ? 1 : 2;
 }
 
+size_t sinkhorn_points_workspace_bytes(const sk_problem *p, int32_t D) {
+    if (check_points(p, D) != SK_OK) return 0;
+    if (points_on_the_fly(p, D)) return sk::tiled_points_workspace_bytes(p->B, p->d1, p->d2);
+    return cost_bytes(p) + sinkhorn_workspace_bytes(p);
+}
+
 size_t sinkhorn_workspace_bytes(const sk_problem *p) {
     if (check_problem(p) != SK_OK) return 0;
     if (sk::resident_fits(p->d1, p->d2)) return 0;
@@ -101,35 +182,8 @@ sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu
     const size_t need = sinkhorn_workspace_bytes(p);
     if (ws_bytes < need) return SK_ERR_WORKSPACE;
     if (need > 0 && !workspace) return SK_ERR_NULLPTR;
-
-    sk::FwdArgs a;
-    a.mu = mu;
-    a.nu = nu;
-    a.C = C;
-    a.alpha = alpha;
-    a.beta = beta;
-    a.loss = loss;
-    a.marg_err = marg_err;
-    a.iters = iters;
-    a.B = p->B;
-    a.d1 = p->d1;
-    a.d2 = p->d2;
-    a.n_iter = p->n_iter;
-    a.c_batched = p->c_batched;
-    a.lambda = p->lambda;
-    a.tol = p->tol;
-    a.s = sk::kLog2eHost / p->lambda;
-
-    a.only_flagged = 0;
-
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if (!sk::resident_fits(p->d1, p->d2)) {
-        e = sk::launch_tiled(a, workspace, s);
-    } else {
-        e = launch_resident_regime(a, resident_form(), s);
-    }
-    return e == hipSuccess ? SK_OK : SK_ERR_HIP;
+    const sk::FwdArgs a = fwd_args(p, mu, nu, C, alpha, beta, loss, marg_err, iters);
+    return run_forward(a, workspace, static_cast<hipStream_t>(stream)) == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 
 sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu,
@@ -141,23 +195,65 @@ sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const f
     if (!grad_loss || !mu || !nu || !alpha || !beta || !grad_mu || !grad_nu) return SK_ERR_NULLPTR;
     if (grad_C && !C) return SK_ERR_NULLPTR;
 
-    sk::BwdArgs a;
-    a.grad_loss = grad_loss;
-    a.mu = mu;
-    a.nu = nu;
-    a.C = C;
-    a.alpha = alpha;
-    a.beta = beta;
-    a.grad_mu = grad_mu;
-    a.grad_nu = grad_nu;
-    a.grad_C = grad_C;
-    a.B = p->B;
-    a.d1 = p->d1;
-    a.d2 = p->d2;
-    a.c_batched = p->c_batched;
-    a.lambda = p->lambda;
-    a.s = sk::kLog2eHost / p->lambda;
+    const sk::BwdArgs a = bwd_args(p, grad_loss, mu, nu, C, alpha, beta, grad_mu, grad_nu, grad_C);
     hipError_t e = sk::launch_backward(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SK_OK : SK_ERR_HIP;
+}
+
+sk_status sinkhorn_forward_points(const sk_problem *p, int32_t D, const float *mu, const float *nu, const float *X,
+                                  const float *Y, float *alpha, float *beta, float *loss, float *marg_err,
+                                  int32_t *iters, void *workspace, size_t ws_bytes, void *stream) {
+    sk_status st = check_points(p, D);
+    if (st != SK_OK) return st;
+    if (p->B == 0) return SK_OK;
+    if (!mu || !nu || !X || !Y || !alpha || !beta || !loss || !marg_err || !iters) return SK_ERR_NULLPTR;
+    const size_t need = sinkhorn_points_workspace_bytes(p, D);
+    if (ws_bytes < need) return SK_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return SK_ERR_NULLPTR;
+    sk::FwdArgs a = fwd_args(p, mu, nu, nullptr, alpha, beta, loss, marg_err, iters);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (points_on_the_fly(p, D)) {
+        e = sk::launch_tiled_points(a, X, Y, D, sqrt((double)a.s), workspace, s);
+    } else {
+        float *C = static_cast<float *>(workspace);
+        e = sk::launch_points_cost(X, Y, C, p->c_batched ? p->B : 1, p->d1, p->d2, D, s);
+        if (e == hipSuccess) {
+            a.C = C;
+            e = run_forward(a, static_cast<char *>(workspace) + cost_bytes(p), s);
+        }
+    }
+    return e == hipSuccess ? SK_OK : SK_ERR_HIP;
+}
+
+sk_status sinkhorn_backward_points(const sk_problem *p, int32_t D, const float *grad_loss, const float *mu,
+                                   const float *nu, const float *X, const float *Y, const float *alpha,
+                                   const float *beta, float *grad_mu, float *grad_nu, float *grad_X, float *grad_Y,
+                                   void *stream) {
+    sk_status st = check_points(p, D);
+    if (st != SK_OK) return st;
+    if (p->B == 0) return SK_OK;
+    if (!grad_loss || !mu || !nu || !alpha || !beta || !grad_mu || !grad_nu) return SK_ERR_NULLPTR;
+    if ((grad_X || grad_Y) && (!X || !Y)) return SK_ERR_NULLPTR;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = sk::launch_backward(bwd_args(p, grad_loss, mu, nu, nullptr, alpha, beta, grad_mu, grad_nu, nullptr), s);
+    if (e == hipSuccess && (grad_X || grad_Y)) {
+        sk::PointsBwdArgs g;
+        g.grad_loss = grad_loss;
+        g.alpha = alpha;
+        g.beta = beta;
+        g.X = X;
+        g.Y = Y;
+        g.grad_X = grad_X;
+        g.grad_Y = grad_Y;
+        g.B = p->B;
+        g.d1 = p->d1;
+        g.d2 = p->d2;
+        g.D = D;
+        g.batched = p->c_batched;
+        g.rs = (float)sqrt((double)(sk::kLog2eHost / p->lambda));
+        e = sk::launch_points_grads(g, s);
+    }
     return e == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 

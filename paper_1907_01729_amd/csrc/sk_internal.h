@@ -57,4 +57,28 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);
 
 hipError_t launch_backward(const BwdArgs &a, hipStream_t st);
 
+// Point clouds (C_ij = sum_k (x_ik - y_jk)^2).  The tiled sweep computes the
+// cost on the fly for per-sample clouds with up to kPointsMaxD coordinates
+// and d2 <= kPointsMaxD2 (the columns' coordinates live in registers); other
+// shapes write the cost out first.  Gradients take up to kPointsGradD
+// coordinates.
+constexpr int kPointsMaxD = 3;
+constexpr int kPointsMaxD2 = 2048;
+constexpr int kPointsGradD = 16;
+
+struct PointsBwdArgs {
+    const float *grad_loss, *alpha, *beta, *X, *Y;
+    float *grad_X, *grad_Y;  // either may be null
+    int B, d1, d2, D, batched;
+    float rs;  // sqrt(log2(e) / lambda)
+};
+
+bool tiled_points_fits(int B, int d1, int d2, int D);
+size_t tiled_points_workspace_bytes(int B, int d1, int d2);
+hipError_t launch_tiled_points(const FwdArgs &a, const float *X, const float *Y, int D, double rs, void *ws,
+                               hipStream_t st);
+hipError_t launch_points_cost(const float *X, const float *Y, float *C, int nb, int d1, int d2, int D,
+                              hipStream_t st);
+hipError_t launch_points_grads(const PointsBwdArgs &a, hipStream_t st);
+
 }  // namespace sk

@@ -40,6 +40,11 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the onl
 
 struct TiledArgs {
     const float *mu, *nu, *C;
+    // Point clouds instead of C (C is then null): X [B, d1, D], Y [B, d2, D];
+    // cl_ij = -|rs x_i - rs y_j|^2 with rs = sqrt(log2(e) / lambda).
+    const float *X, *Y;
+    int D;
+    float rs;
     float *a;        // [B, d1] base-2 potentials (the alpha output buffer)
     float *a2;       // [B, d1] second plane of the potentials (streaming sweep: odd iterations), or null
     float *bbuf;     // [2][B, d2p] base-2 column potentials, ping-pong by iteration parity
@@ -89,6 +94,22 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
         T.state[u] = 0;
 }
 
+// Scaled cost of one cell from the point clouds: -sum_k (rs x_ik - rs y_jk)^2,
+// accumulated in coordinate order (the points sweep computes the same bits).
+__device__ __forceinline__ float cl_points(const TiledArgs &T, int b, int i, int j) {
+    const float *x = T.X + ((size_t)b * T.d1 + i) * T.D;
+    const float *y = T.Y + ((size_t)b * T.d2 + j) * T.D;
+    float acc = 0.f;
+    for (int k = 0; k < T.D; ++k) {
+        const float dd = T.rs * x[k] - T.rs * y[k];
+        acc = __builtin_fmaf(dd, dd, acc);
+    }
+    return -acc;
+}
+__device__ __forceinline__ float cl_at(const TiledArgs &T, const float *Cb, int b, int i, int j) {
+    return T.X ? cl_points(T, b, i, j) : -T.s * Cb[(size_t)i * T.d2 + j];
+}
+
 // v-update of iteration 1, per row block: online (max, sumexp) of
 // a^0_i + cl_ij over the block's rows for every column j (one thread per
 // (problem, column), reading cost rows coalesced across threads).
@@ -97,12 +118,12 @@ __global__ __launch_bounds__(kMergeThreads) void sk_tiled_col_exact(TiledArgs T)
     const int r = blockIdx.y, b = blockIdx.z;
     if (j >= T.d2) return;
     const int i0 = r * T.RBS, i1 = min(T.d1, i0 + T.RBS);
-    const float *Cb = T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0);
+    const float *Cb = T.C ? T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0) : nullptr;
     const float *mub = T.mu + (size_t)b * T.d1;
     float m = kNegBig, s = 0.f;
     for (int i = i0; i < i1; ++i) {
         if (!(mub[i] > 0.f)) continue;  // a^0 = -inf: contributes nothing
-        const float x = -T.s * Cb[(size_t)i * T.d2 + j];
+        const float x = cl_at(T, Cb, b, i, j);
         const float mn = fmaxf(m, x);
         s = s * ex2(m - mn) + ex2(x - mn);
         m = mn;
@@ -114,13 +135,13 @@ __global__ __launch_bounds__(kMergeThreads) void sk_tiled_col_exact(TiledArgs T)
 // Exact logsumexp (base 2) over all rows i of a_i + cl_ij for one column:
 // the fallback of the merge when the shifted column sum left [2^-64, 2^64].
 __device__ float col_lse_exact(const TiledArgs &T, int b, int j) {
-    const float *Cb = T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0);
+    const float *Cb = T.C ? T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0) : nullptr;
     const float *ab = T.a + (size_t)b * T.d1;
     float m = neg_inf();
-    for (int i = 0; i < T.d1; ++i) m = fmaxf(m, ab[i] - T.s * Cb[(size_t)i * T.d2 + j]);
+    for (int i = 0; i < T.d1; ++i) m = fmaxf(m, ab[i] + cl_at(T, Cb, b, i, j));
     if (m == neg_inf()) return m;
     float s = 0.f;
-    for (int i = 0; i < T.d1; ++i) s += ex2(ab[i] - T.s * Cb[(size_t)i * T.d2 + j] - m);
+    for (int i = 0; i < T.d1; ++i) s += ex2(ab[i] + cl_at(T, Cb, b, i, j) - m);
     return m + lg2(s);
 }
 
@@ -312,6 +333,116 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
 #pragma unroll
         for (int q = 0; q < kWaves; ++q) s += lds[q * NCW * 64 + j];
         T.part[pidx(T, 0, r, b, j)] = s;
+    }
+    if (threadIdx.x == 0) {
+        float re = 0.f, lo = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) {
+            re += scal[q];
+            lo += scal[kWaves + q];
+        }
+        const int plane = STATS ? 2 : (k & 1);
+        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
+        if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
+    }
+}
+
+// Cost of the lane's columns from point coordinates held in registers: the
+// row's scaled coordinates xs against the columns' ys (padding columns sit
+// at kFarCoord: cl = -3e36, plan entry 0, 0 * cl finite).
+constexpr float kFarCoord = 1.0e18f;
+template <int NCW, int D>
+struct PointsCost {
+    const float (&ys)[NCW][D];
+    const float (&xs)[D];
+    __device__ __forceinline__ float operator()(int c) const {
+        float acc = 0.f;
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+            const float dd = xs[k] - ys[c][k];
+            acc = __builtin_fmaf(dd, dd, acc);
+        }
+        return -acc;
+    }
+};
+
+// Sweep over per-sample point clouds (the on-the-fly cost of Section 4's
+// closing remark: cost entries are recreated from the points, no cost matrix
+// exists).  Work-group (row block r, problem b) as in sk_tiled_sweep; lane l
+// keeps the scaled coordinates of its columns j = l + 64 c in registers.  The
+// row's coordinates, potential and mass are loaded one row ahead through a
+// lane-varying index, so they arrive in vector registers (vector operands
+// taken from scalar registers issue at half rate on this chip).
+template <int NCW, int D, bool STATS>
+__global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, int k) {
+    extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
+    __shared__ float scal[2 * kWaves];
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int d1 = T.d1, d2 = T.d2;
+
+    const int st = T.state[b];
+    if (!STATS) {
+        if (st != 0) return;
+        if (stop_before(T, b, k)) {
+            if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
+            return;
+        }
+    }
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
+    float *ab = T.a + (size_t)b * d1;
+    const float *mub = T.mu + (size_t)b * d1;
+    const float *xb = T.X + (size_t)b * d1 * D;
+    const float *yb = T.Y + (size_t)b * d2 * D;
+    const float rs = T.rs;
+
+    float bv[NCW], colpart[NCW], ys[NCW][D];
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const int j = lane + 64 * c;
+        bv[c] = bsrc[j];  // 0 past d2 (padded stride)
+        colpart[c] = 0.f;
+#pragma unroll
+        for (int q = 0; q < D; ++q) ys[c][q] = j < d2 ? rs * yb[(size_t)j * D + q] : kFarCoord;
+    }
+    int vz = 0;
+    __asm__ volatile("" : "+v"(vz));  // a zero the compiler cannot see as uniform
+    float xn[D], an = 0.f, mn = 0.f;
+    auto load_row = [&](int i) {
+        const int ii = i + vz;
+#pragma unroll
+        for (int q = 0; q < D; ++q) xn[q] = rs * xb[(size_t)ii * D + q];
+        an = ab[ii];
+        mn = mub[ii];
+    };
+    float rowerr = 0.f, losspart = 0.f;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    if (i0 + w < i1) load_row(i0 + w);
+    for (int i = i0 + w; i < i1; i += kWaves) {
+        float xs[D];
+#pragma unroll
+        for (int q = 0; q < D; ++q) xs[q] = xn[q];
+        const float ai = an, mui = mn;
+        if (i + kWaves < i1) load_row(i + kWaves);  // another row of this wavefront: no conflict with the store below
+        const PointsCost<NCW, D> cost{ys, xs};
+        row_step<NCW, STATS>(cost, ai, mui, ab + i, bv, colpart, rowerr, losspart, lane);
+    }
+
+    // Combine the wavefronts' partials in LDS, fixed order, and store.
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) lds[w * NCW * 64 + c * 64 + lane] = colpart[c];
+    const float lw = STATS ? wave_sum(losspart) : 0.f;
+    if (lane == 0) {
+        scal[w] = rowerr;
+        scal[kWaves + w] = lw;
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < d2; j += kThreads) {
+        float sum = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) sum += lds[q * NCW * 64 + j];
+        T.part[pidx(T, 0, r, b, j)] = sum;
     }
     if (threadIdx.x == 0) {
         float re = 0.f, lo = 0.f;
@@ -957,11 +1088,15 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
     }
 }
 
+// Cost kinds of the tiled regime: a shared cost, a per-sample cost, per-sample
+// point clouds (cost computed on the fly).
+constexpr int kKindShared = 0, kKindBatched = 1, kKindPoints = 2;
+
 // Which sweep serves a problem: the shared-cost sweep with W problems per
 // work-group when C is shared and the batch fills at least four wavefronts,
 // otherwise one problem per work-group.
-int shared_width(int B, int c_batched) {
-    if (c_batched) return 0;
+int shared_width(int B, int kind) {
+    if (kind != kKindShared) return 0;
     if (B >= 8) return 8;
     if (B >= 4) return 4;
     return 0;
@@ -971,13 +1106,13 @@ int shared_width(int B, int c_batched) {
 // wavefronts, rows per block a multiple of the wavefronts per group.  Shared
 // cost: ~256 (wide rows) or ~512 work-groups, the count of row blocks a
 // multiple of 8 when the rows allow it so that a row block stays on one XCD.
-bool stream_shape(int d2, int c_batched);
+bool stream_shape(int d2, int kind);
 int stream_waves(int d2);
 
-void row_blocks(int B, int d1, int d2, int c_batched, int *R, int *RBS) {
-    const int W = shared_width(B, c_batched);
+void row_blocks(int B, int d1, int d2, int kind, int *R, int *RBS) {
+    const int W = shared_width(B, kind);
     int want, unit;
-    if (stream_shape(d2, c_batched)) {
+    if (stream_shape(d2, kind)) {
         // Streaming sweep: about one work-group per CU, and at most
         // 64 kSegs rows per wavefront (row potentials held in registers).
         want = (256 + B - 1) / (B > 0 ? B : 1);
@@ -1023,20 +1158,20 @@ int nc4_bucket(int d2) {
     const int n = (d2 + 255) / 256;
     return n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
 }
-bool stream_shape(int d2, int c_batched) { return c_batched && d2 % 4 == 0; }
+bool stream_shape(int d2, int kind) { return kind == kKindBatched && d2 % 4 == 0; }
 int stream_nc4(int d2) { return (d2 + 255) / 256; }
 int stream_waves(int d2) { return stream_nc4(d2) <= 8 ? 4 : 2; }
-int padded_width(int d2, int c_batched) {
+int padded_width(int d2, int kind) {
     int w = 64 * ncw_bucket(d2);
-    if (stream_shape(d2, c_batched)) w = w > 256 * nc4_bucket(d2) ? w : 256 * nc4_bucket(d2);
+    if (stream_shape(d2, kind)) w = w > 256 * nc4_bucket(d2) ? w : 256 * nc4_bucket(d2);
     return w;
 }
 
-Layout layout(int B, int d1, int d2, int c_batched, int *R_out, int *RBS_out, int *JC_out) {
+Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC_out) {
     int R, RBS;
-    row_blocks(B, d1, d2, c_batched, &R, &RBS);
+    row_blocks(B, d1, d2, kind, &R, &RBS);
     const int JC = (d2 + kMergeThreads - 1) / kMergeThreads;
-    const size_t d2p = padded_width(d2, c_batched);
+    const size_t d2p = padded_width(d2, kind);
     Layout L;
     size_t off = 0;
     L.bbuf = off;
@@ -1052,7 +1187,7 @@ Layout layout(int B, int d1, int d2, int c_batched, int *R_out, int *RBS_out, in
     L.state = off;
     off = align256(off + sizeof(int32_t) * (size_t)B);
     L.a2 = off;
-    if (stream_shape(d2, c_batched)) off = align256(off + sizeof(float) * (size_t)B * d1);
+    if (stream_shape(d2, kind)) off = align256(off + sizeof(float) * (size_t)B * d1);
     L.total = off;
     if (R_out) *R_out = R;
     if (RBS_out) *RBS_out = RBS;
@@ -1145,6 +1280,24 @@ hipError_t run_shared(const TiledArgs &T, hipStream_t st) {
         [&]() { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>), grid, blk, lds, st, T, 0); });
 }
 
+template <int NCW, int D>
+hipError_t run_points(const TiledArgs &T, hipStream_t st) {
+    const size_t lds = sizeof(float) * kWaves * NCW * 64;
+    const dim3 grid(T.R, T.B), blk(kThreads);
+    return run_sequence(
+        T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_points<NCW, D, false>), grid, blk, lds, st, T, k); },
+        [&]() { hipLaunchKernelGGL((sk_tiled_sweep_points<NCW, D, true>), grid, blk, lds, st, T, 0); });
+}
+
+template <int D>
+hipError_t dispatch_points(const TiledArgs &T, int ncw, hipStream_t st) {
+    if (ncw <= 4) return run_points<4, D>(T, st);
+    if (ncw <= 8) return run_points<8, D>(T, st);
+    if (ncw <= 13) return run_points<13, D>(T, st);
+    if (ncw <= 16) return run_points<16, D>(T, st);
+    return run_points<32, D>(T, st);
+}
+
 template <bool BATCHED>
 hipError_t dispatch(const TiledArgs &T, int ncw, hipStream_t st) {
     if (ncw <= 4) return run<4, BATCHED>(T, st);
@@ -1168,23 +1321,40 @@ hipError_t dispatch_shared(const TiledArgs &T, int ncw, hipStream_t st) {
 }  // namespace
 
 size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched) {
-    return layout(B, d1, d2, c_batched, nullptr, nullptr, nullptr).total;
+    return layout(B, d1, d2, c_batched ? kKindBatched : kKindShared, nullptr, nullptr, nullptr).total;
 }
 
 bool tiled_fits(int B, int d1, int d2, int c_batched) {
     int R, RBS;
-    row_blocks(B, d1, d2, c_batched, &R, &RBS);
+    row_blocks(B, d1, d2, c_batched ? kKindBatched : kKindShared, &R, &RBS);
     return d2 <= kTiledMaxD2 && B <= 65535 && R <= 65535;
 }
 
-hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
+bool tiled_points_fits(int B, int d1, int d2, int D) {
+    int R, RBS;
+    row_blocks(B, d1, d2, kKindPoints, &R, &RBS);
+    return D >= 1 && D <= kPointsMaxD && d2 <= kPointsMaxD2 && B <= 65535 && R <= 65535;
+}
+
+size_t tiled_points_workspace_bytes(int B, int d1, int d2) {
+    return layout(B, d1, d2, kKindPoints, nullptr, nullptr, nullptr).total;
+}
+
+namespace {
+// Workspace carving and scalar arguments common to every tiled launch.
+TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     TiledArgs T;
     int R, RBS, JC;
-    const Layout L = layout(a.B, a.d1, a.d2, a.c_batched, &R, &RBS, &JC);
+    const Layout L = layout(a.B, a.d1, a.d2, kind, &R, &RBS, &JC);
+    *Lout = L;
     char *base = static_cast<char *>(ws);
     T.mu = a.mu;
     T.nu = a.nu;
     T.C = a.C;
+    T.X = nullptr;
+    T.Y = nullptr;
+    T.D = 0;
+    T.rs = 0.f;
     T.a = a.alpha;
     T.a2 = nullptr;
     T.bbuf = reinterpret_cast<float *>(base + L.bbuf);
@@ -1201,21 +1371,46 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     T.B = a.B;
     T.d1 = a.d1;
     T.d2 = a.d2;
-    T.d2p = padded_width(a.d2, a.c_batched);
+    T.d2p = padded_width(a.d2, kind);
     T.R = R;
     T.RBS = RBS;
     T.JC = JC;
     T.n_iter = a.n_iter;
-    T.c_batched = a.c_batched;
+    T.c_batched = kind != kKindShared;
     T.s = a.s;
     T.tol = a.tol;
+    return T;
+}
+}  // namespace
+
+hipError_t launch_tiled_points(const FwdArgs &a, const float *X, const float *Y, int D, double rs, void *ws,
+                               hipStream_t st) {
+    Layout L;
+    TiledArgs T = tiled_args(a, kKindPoints, ws, &L);
+    T.C = nullptr;
+    T.X = X;
+    T.Y = Y;
+    T.D = D;
+    T.rs = (float)rs;
+    const int ncw = (a.d2 + 63) / 64;
+    switch (D) {
+        case 1: return dispatch_points<1>(T, ncw, st);
+        case 2: return dispatch_points<2>(T, ncw, st);
+        default: return dispatch_points<3>(T, ncw, st);
+    }
+}
+
+hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
+    Layout L;
+    TiledArgs T = tiled_args(a, a.c_batched ? kKindBatched : kKindShared, ws, &L);
+    char *base = static_cast<char *>(ws);
     const int ncw = (a.d2 + 63) / 64;
     const int W = shared_width(a.B, a.c_batched);
     // 16-byte global->LDS copies need 16-byte aligned cost rows.
     const bool vec4 = a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0;
     if (W == 8) return vec4 ? dispatch_shared<8, true>(T, ncw, st) : dispatch_shared<8, false>(T, ncw, st);
     if (W == 4) return vec4 ? dispatch_shared<4, true>(T, ncw, st) : dispatch_shared<4, false>(T, ncw, st);
-    if (stream_shape(a.d2, a.c_batched) && ((uintptr_t)a.C % 16) == 0) {
+    if (stream_shape(a.d2, a.c_batched ? kKindBatched : kKindShared) && ((uintptr_t)a.C % 16) == 0) {
         T.a2 = reinterpret_cast<float *>(base + L.a2);
         switch (stream_nc4(a.d2)) {
             case 1: return run_stream<1>(T, st);

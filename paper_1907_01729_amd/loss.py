@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import torch
 
-from ._binding import sinkhorn_backward, sinkhorn_forward
+from ._binding import sinkhorn_backward, sinkhorn_backward_points, sinkhorn_forward, sinkhorn_forward_points
 
 
 class SinkhornLoss(torch.autograd.Function):
@@ -36,6 +36,38 @@ class SinkhornLoss(torch.autograd.Function):
 def sinkhorn_loss(mu, nu, C, lam, n_iter, tol=0.0, return_state=False):
     """Per-sample loss E^0 [B]; differentiable w.r.t. mu, nu and C."""
     loss, alpha, beta, merr, iters = SinkhornLoss.apply(mu, nu, C, lam, n_iter, tol)
+    if return_state:
+        return loss, dict(alpha=alpha, beta=beta, marg_err=merr, iters=iters)
+    return loss
+
+
+class SinkhornPointsLoss(torch.autograd.Function):
+    """The same loss with the cost given by point clouds, C_ij = |X_i - Y_j|^2;
+    the gradient reaches the points through dW/dC = P (chain rule)."""
+
+    @staticmethod
+    def forward(ctx, mu, nu, X, Y, lam, n_iter, tol):
+        out = sinkhorn_forward_points(mu.contiguous(), nu.contiguous(), X.contiguous(), Y.contiguous(), lam, n_iter,
+                                      tol)
+        ctx.save_for_backward(mu, nu, X, Y, out["alpha"], out["beta"])
+        ctx.lam = lam
+        ctx.mark_non_differentiable(out["alpha"], out["beta"], out["marg_err"], out["iters"])
+        return out["loss"], out["alpha"], out["beta"], out["marg_err"], out["iters"]
+
+    @staticmethod
+    def backward(ctx, grad_loss, *unused):
+        mu, nu, X, Y, alpha, beta = ctx.saved_tensors
+        want = ctx.needs_input_grad[2] or ctx.needs_input_grad[3]
+        g = sinkhorn_backward_points(grad_loss.contiguous(), mu.contiguous(), nu.contiguous(), X.contiguous(),
+                                     Y.contiguous(), ctx.lam, alpha, beta, grad_points=want)
+        gX = g["grad_X"].reshape(X.shape) if want and ctx.needs_input_grad[2] else None
+        gY = g["grad_Y"].reshape(Y.shape) if want and ctx.needs_input_grad[3] else None
+        return g["grad_mu"], g["grad_nu"], gX, gY, None, None, None
+
+
+def sinkhorn_loss_points(mu, nu, X, Y, lam, n_iter, tol=0.0, return_state=False):
+    """Per-sample loss E^0 [B] for point clouds; differentiable w.r.t. mu, nu, X and Y."""
+    loss, alpha, beta, merr, iters = SinkhornPointsLoss.apply(mu, nu, X, Y, lam, n_iter, tol)
     if return_state:
         return loss, dict(alpha=alpha, beta=beta, marg_err=merr, iters=iters)
     return loss

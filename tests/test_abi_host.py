@@ -102,3 +102,43 @@ def test_workspace_too_small_rejected_before_launch():
     assert need > 0
     # non-NULL (never dereferenced) pointers so that only the size check fires
     assert _fwd(p, ptr=0x1000, ws=need - 1) == -5
+
+
+def _fwd_points(p, D, ptr=None, ws=0):
+    lib = sk.load_library()
+    v = ctypes.c_void_p(ptr) if ptr else None
+    return lib.sinkhorn_forward_points(ctypes.byref(p), D, v, v, v, v, v, v, v, v, v, v, ctypes.c_size_t(ws), None)
+
+
+def _bwd_points(p, D, ptr=None):
+    lib = sk.load_library()
+    v = ctypes.c_void_p(ptr) if ptr else None
+    return lib.sinkhorn_backward_points(ctypes.byref(p), D, v, v, v, v, v, v, v, v, v, None, None, None)
+
+
+def test_points_rejections_on_host():
+    p = _binding.problem(4, 300, 500, 1, 0.1, 10)
+    for D in (0, -1, 17):
+        assert _fwd_points(p, D) == -2
+        assert _bwd_points(p, D) == -2
+        assert sk.sinkhorn_points_workspace_bytes(4, 300, 500, 1, D, 0.1, 10) == 0
+    assert _fwd_points(p, 3) == -1
+    assert _bwd_points(p, 3) == -1
+    assert _fwd_points(_binding.problem(4, 300, 500, 1, 0.0, 10), 3) == -3
+    assert _fwd_points(_binding.problem(0, 300, 500, 1, 0.1, 10), 3) == 0
+    need = sk.sinkhorn_points_workspace_bytes(4, 300, 500, 1, 3, 0.1, 10)
+    assert need > 0
+    assert _fwd_points(p, 3, ptr=0x1000, ws=need - 1) == -5
+
+
+def test_points_workspace_sizes():
+    # on-the-fly sweep (per-sample clouds, tiled shape, D <= 3, d2 <= 2048): no cost matrix in the workspace
+    on_the_fly = sk.sinkhorn_points_workspace_bytes(32, 1024, 2048, 1, 3, 0.05, 100)
+    assert 0 < on_the_fly < 32 * 1024 * 2048 * 4
+    # everything else holds the cost matrix written out, then the forward's own workspace
+    cost = 32 * 1024 * 2048 * 4
+    assert sk.sinkhorn_points_workspace_bytes(32, 1024, 2048, 1, 4, 0.05, 100) >= cost
+    assert sk.sinkhorn_points_workspace_bytes(32, 100, 100, 1, 3, 0.05, 100) >= 32 * 100 * 100 * 4
+    assert sk.sinkhorn_points_workspace_bytes(32, 1024, 2100, 1, 3, 0.05, 100) >= 32 * 1024 * 2100 * 4
+    shared = sk.sinkhorn_points_workspace_bytes(32, 784, 784, 0, 2, 0.01, 100)
+    assert shared >= 784 * 784 * 4 + sk.sinkhorn_workspace_bytes(32, 784, 784, 0, 0.01, 100)

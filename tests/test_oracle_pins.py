@@ -16,6 +16,7 @@ import pytest
 from scipy.optimize import minimize
 
 import oracle
+import workloads
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -461,3 +462,65 @@ def test_planted_mistakes_are_caught(mutation):
     W, f, g = _scipy_dual(mu, nu, C, lam)
     dual_ok = abs(lam * (a2 @ mu + b2 @ nu) - W) < 1e-6
     assert not (finite_k_ok and dual_ok), mutation
+
+
+# --------------------------------------------------------------------------
+# Point clouds: the cost recreated from coordinates (Section 4's closing
+# remark) and the gradient with respect to the points (chain rule through
+# dW/dC = P)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("D", [1, 2, 3, 5])
+def test_cost_from_points_matches_cdist(D):
+    """The oracle's squared distances equal scipy's cdist('sqeuclidean') (an
+    independent library routine), per cloud pair."""
+    from scipy.spatial.distance import cdist
+    p = workloads.random_points(40 + D, B=3, d1=7, d2=11, D=D, lam=0.1, n_iter=1, offset=3.0)
+    C = oracle.cost_from_points(p.X, p.Y)
+    for b in range(3):
+        ref = cdist(p.X[b].astype(np.float64), p.Y[b].astype(np.float64), "sqeuclidean")
+        np.testing.assert_allclose(C[b], ref, rtol=1e-12, atol=1e-12)
+
+
+def _points_grads_fd_case(mutation=None):
+    rng = np.random.default_rng(23)
+    d1, d2, D, lam = 4, 5, 2, 0.3
+    mu, nu = _rand_hist(rng, d1), _rand_hist(rng, d2)
+    X = rng.standard_normal((d1, D))
+    Y = rng.standard_normal((d2, D)) + 0.5
+    C = oracle.cost_from_points(X, Y)[0]
+    _, o = _W(mu, nu, C, lam)
+    G = oracle.backward([1.0], mu, nu, C, lam, o["alpha"], o["beta"], grad_C=True)["grad_C"]
+    gX, gY = oracle.points_grads(G, X, Y)
+    if mutation == "sign":
+        gX = -gX
+    elif mutation == "factor":
+        gX = 0.5 * gX
+    h = 1e-6
+    ok = True
+    for (i, k) in [(0, 0), (2, 1), (3, 0)]:
+        E = np.zeros_like(X); E[i, k] = 1.0
+        fd = (_W(mu, nu, oracle.cost_from_points(X + h * E, Y)[0], lam)[0]
+              - _W(mu, nu, oracle.cost_from_points(X - h * E, Y)[0], lam)[0]) / (2 * h)
+        ok &= abs(fd - gX[0, i, k]) <= 1e-6 * max(1.0, abs(fd))
+    for (j, k) in [(1, 1), (4, 0)]:
+        E = np.zeros_like(Y); E[j, k] = 1.0
+        fd = (_W(mu, nu, oracle.cost_from_points(X, Y + h * E)[0], lam)[0]
+              - _W(mu, nu, oracle.cost_from_points(X, Y - h * E)[0], lam)[0]) / (2 * h)
+        ok &= abs(fd - gY[0, j, k]) <= 1e-6 * max(1.0, abs(fd))
+    return ok, gX, gY
+
+
+def test_fd_gradient_points():
+    """d W_lambda / d X and d Y by central differences of the converged dual
+    match the chain rule through dW/dC = P; translating both clouds together
+    leaves C unchanged, so the gradients sum to zero over all points."""
+    ok, gX, gY = _points_grads_fd_case()
+    assert ok
+    np.testing.assert_allclose(gX.sum(axis=(0, 1)) + gY.sum(axis=(0, 1)), 0.0, atol=1e-12)
+
+
+@pytest.mark.parametrize("mutation", ["sign", "factor"])
+def test_points_grads_planted_mistakes_are_caught(mutation):
+    ok, _, _ = _points_grads_fd_case(mutation)
+    assert not ok

@@ -146,6 +146,80 @@ def clouds(seed=1005, B=32, d1=1024, d2=2048, n_iter=100, lam=0.05):
                    grad_C=True)
 
 
+@dataclass
+class PointsProblem:
+    """A batch whose cost is given by point clouds: C_ij = |X_i - Y_j|^2
+    (X [1 or B, d1, D], Y [1 or B, d2, D]; the cost itself is not drawn)."""
+    name: str
+    mu: np.ndarray        # [B, d1] float32
+    nu: np.ndarray        # [B, d2] float32
+    X: np.ndarray         # [1 or B, d1, D] float32
+    Y: np.ndarray         # [1 or B, d2, D] float32
+    lam: float
+    n_iter: int
+    tol: float = 0.0
+    grad_points: bool = False
+
+    @property
+    def B(self):
+        return self.mu.shape[0]
+
+    @property
+    def d1(self):
+        return self.mu.shape[1]
+
+    @property
+    def d2(self):
+        return self.nu.shape[1]
+
+    @property
+    def D(self):
+        return self.X.shape[2]
+
+    @property
+    def c_batched(self):
+        return self.X.shape[0] != 1
+
+
+def clouds_points(seed=1005, B=32, d1=1024, d2=2048, n_iter=100, lam=0.05):
+    """The point-cloud workload with the cost left implicit: the same draws as
+    clouds() (x ~ N(0, I_3)^d1, y ~ N(0, I_3)^d2 + s_b), stored as float32
+    coordinates X[b] = x, Y[b] = y + s_b; uniform mu, nu; lambda 0.05."""
+    rng = np.random.default_rng(seed)
+    X = np.empty((B, d1, 3))
+    Y = np.empty((B, d2, 3))
+    for b in range(B):
+        X[b] = rng.standard_normal((d1, 3))
+        y = rng.standard_normal((d2, 3))
+        Y[b] = y + rng.standard_normal(3)
+    mu = np.full((B, d1), 1.0 / d1)
+    nu = np.full((B, d2), 1.0 / d2)
+    return PointsProblem("clouds_points", mu.astype(np.float32), nu.astype(np.float32), X.astype(np.float32),
+                         Y.astype(np.float32), lam, n_iter, grad_points=True)
+
+
+def random_points(seed, B, d1, d2, D, lam, n_iter, batched=True, zero_frac=0.0, tol=0.0, scale=1.0,
+                  offset=0.0):
+    """Generic point-cloud problem: positive histograms (optionally with a
+    fraction of exact zeros, one non-zero kept per sample), X ~ scale*N(0,I_D)
+    and Y ~ scale*N(0,I_D) + scale*N(0,I_D) shift per cloud, both moved by
+    `offset` (tests translation robustness)."""
+    rng = np.random.default_rng(seed)
+    mu = rng.uniform(0.05, 1.0, size=(B, d1))
+    nu = rng.uniform(0.05, 1.0, size=(B, d2))
+    if zero_frac > 0:
+        for h in (mu, nu):
+            z = rng.random(h.shape) < zero_frac
+            z[:, 0] = False
+            h[z] = 0.0
+    mu, nu = _normalise(mu), _normalise(nu)
+    nc = B if batched else 1
+    X = scale * rng.standard_normal((nc, d1, D)) + offset
+    Y = scale * (rng.standard_normal((nc, d2, D)) + rng.standard_normal((nc, 1, D))) + offset
+    return PointsProblem(f"points{seed}", mu.astype(np.float32), nu.astype(np.float32), X.astype(np.float32),
+                         Y.astype(np.float32), lam, n_iter, tol=tol)
+
+
 CONFIGS = {
     1: tiny,
     2: label,
