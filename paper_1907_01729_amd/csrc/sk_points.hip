@@ -130,6 +130,121 @@ __global__ __launch_bounds__(kPtThreads) void sk_points_grad_y(PointsBwdArgs A) 
         if (k < D) A.grad_Y[((size_t)bx * A.d2 + j) * D + k] = acc[k];
 }
 
+// One side's point gradient for per-sample clouds, as a sweep over that
+// side's points ("rows"; the other side's points are the "columns"):
+//   out[b, i] = 2 g_b sum_j P_ij (r_i - c_j),
+//   P_ij = 2^(a_i + b_j - |rs r_i - rs c_j|^2)   (a, b: base-2 potentials).
+// Called once with (X, Y, alpha, beta) for grad_X and once with the roles
+// swapped for grad_Y (P is the same in both roles).  Work-group (row block,
+// problem), wavefront per row; lane l keeps the scaled coordinates and the
+// potentials of its columns j = l + 64 c in registers; a row's coordinates
+// and potential arrive one row ahead in vector registers.  Each row is
+// finished by one wavefront (three wavefront sums), so no cross-work-group
+// reduction and no workspace is needed.
+struct GradSweepArgs {
+    const float *rows, *cols;  // [B, nr, D], [B, nc, D]
+    const float *pr, *pc;      // natural-log potentials [B, nr], [B, nc]
+    const float *grad_loss;    // [B]
+    float *out;                // [B, nr, D]
+    int nr, nc, RBS;
+    float rs;
+};
+constexpr float kFarCoord = 1.0e18f;  // padding columns: cl = -3e36, P = 0
+
+template <int NCW, int D>
+__global__ __launch_bounds__(kPtThreads) void sk_points_grad_sweep(GradSweepArgs A) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int b = blockIdx.y;
+    const int nr = A.nr, nc = A.nc;
+    const float rs = A.rs;
+    const float *rb = A.rows + (size_t)b * nr * D;
+    const float *cb = A.cols + (size_t)b * nc * D;
+    const float *pr = A.pr + (size_t)b * nr;
+    // Raw column values first (clamped index: all loads in flight together).
+    float ys[NCW][D], bv[NCW];
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const int jj = min(lane + 64 * c, nc - 1);
+        bv[c] = A.pc[(size_t)b * nc + jj];
+#pragma unroll
+        for (int q = 0; q < D; ++q) ys[c][q] = cb[(size_t)jj * D + q];
+    }
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const bool in = lane + 64 * c < nc;
+        bv[c] = in ? bv[c] * kLog2e : 0.f;
+#pragma unroll
+        for (int q = 0; q < D; ++q) ys[c][q] = in ? rs * ys[c][q] : kFarCoord;
+    }
+    const float g2 = 2.f * A.grad_loss[b] / rs;  // the sums below are in scaled coordinates
+    int vz = 0;
+    __asm__ volatile("" : "+v"(vz));  // a zero the compiler cannot see as uniform
+    float xn[D], an = 0.f;
+    const int i0 = blockIdx.x * A.RBS, i1 = min(nr, i0 + A.RBS);
+    auto load_row = [&](int i) {  // raw values: the arithmetic waits for the next row
+        const int ii = min(i, i1 - 1) + vz;  // clamped: the prefetch past the block re-reads its last row
+#pragma unroll
+        for (int q = 0; q < D; ++q) xn[q] = rb[(size_t)ii * D + q];
+        an = pr[ii];
+    };
+    const int step = kPtThreads / 64;
+    if (i0 + w < i1) load_row(i0 + w);
+    for (int i = i0 + w; i < i1; i += step) {
+        float xs[D];
+#pragma unroll
+        for (int q = 0; q < D; ++q) xs[q] = rs * xn[q];
+        const float ai = an * kLog2e;
+        load_row(i + step);
+        float gq[D];
+#pragma unroll
+        for (int q = 0; q < D; ++q) gq[q] = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) {
+            float dd[D], acc = 0.f;
+#pragma unroll
+            for (int q = 0; q < D; ++q) {
+                dd[q] = xs[q] - ys[c][q];
+                acc = __builtin_fmaf(dd[q], dd[q], acc);
+            }
+            const float e = ex2((ai + bv[c]) - acc);
+#pragma unroll
+            for (int q = 0; q < D; ++q) gq[q] = __builtin_fmaf(e, dd[q], gq[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            const float v = wave_sum(gq[q]);
+            if (lane == 0) A.out[((size_t)b * nr + i) * D + q] = g2 * v;
+        }
+    }
+}
+
+template <int D>
+void grad_sweep(const GradSweepArgs &g, int B, hipStream_t st) {
+    const dim3 grid((g.nr + g.RBS - 1) / g.RBS, B), blk(kPtThreads);
+    const int ncw = (g.nc + 63) / 64;
+    if (ncw <= 4) hipLaunchKernelGGL((sk_points_grad_sweep<4, D>), grid, blk, 0, st, g);
+    else if (ncw <= 8) hipLaunchKernelGGL((sk_points_grad_sweep<8, D>), grid, blk, 0, st, g);
+    else if (ncw <= 16) hipLaunchKernelGGL((sk_points_grad_sweep<16, D>), grid, blk, 0, st, g);
+    else hipLaunchKernelGGL((sk_points_grad_sweep<32, D>), grid, blk, 0, st, g);
+}
+
+void grad_sweep_side(const PointsBwdArgs &a, bool side_x, hipStream_t st) {
+    GradSweepArgs g;
+    g.rows = side_x ? a.X : a.Y;
+    g.cols = side_x ? a.Y : a.X;
+    g.pr = side_x ? a.alpha : a.beta;
+    g.pc = side_x ? a.beta : a.alpha;
+    g.grad_loss = a.grad_loss;
+    g.out = side_x ? a.grad_X : a.grad_Y;
+    g.nr = side_x ? a.d1 : a.d2;
+    g.nc = side_x ? a.d2 : a.d1;
+    g.RBS = 64;  // 16 rows per wavefront: the columns' registers are loaded once per 16 rows
+    g.rs = a.rs;
+    if (a.D == 1) grad_sweep<1>(g, a.B, st);
+    else if (a.D == 2) grad_sweep<2>(g, a.B, st);
+    else grad_sweep<3>(g, a.B, st);
+}
+
 }  // namespace
 
 hipError_t launch_points_cost(const float *X, const float *Y, float *C, int nb, int d1, int d2, int D,
@@ -142,6 +257,13 @@ hipError_t launch_points_cost(const float *X, const float *Y, float *C, int nb, 
 }
 
 hipError_t launch_points_grads(const PointsBwdArgs &a, hipStream_t st) {
+    // Per-sample clouds with few coordinates: row sweeps with the other side
+    // in registers (both sides at most 2048 points).
+    if (a.batched && a.D <= kPointsMaxD && a.d1 <= kPointsMaxD2 && a.d2 <= kPointsMaxD2 && a.B <= 65535) {
+        if (a.grad_X) grad_sweep_side(a, true, st);
+        if (a.grad_Y) grad_sweep_side(a, false, st);
+        return hipGetLastError();
+    }
     const int wpb = kPtThreads / 64;
     const size_t nb = a.batched ? a.B : 1;
     if (a.grad_X) {

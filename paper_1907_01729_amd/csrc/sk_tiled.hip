@@ -41,8 +41,11 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the onl
 struct TiledArgs {
     const float *mu, *nu, *C;
     // Point clouds instead of C (C is then null): X [B, d1, D], Y [B, d2, D];
-    // cl_ij = -|rs x_i - rs y_j|^2 with rs = sqrt(log2(e) / lambda).
+    // cl_ij = -|rs x_i - rs y_j|^2 with rs = sqrt(log2(e) / lambda), evaluated
+    // as 2 x'.y' - |x'|^2 - |y'|^2 on coordinates x' = rs (x - c_b) centred on
+    // the problem's mean point c_b (ctr, [B][4], computed by sk_tiled_center).
     const float *X, *Y;
+    float *ctr;
     int D;
     float rs;
     float *a;        // [B, d1] base-2 potentials (the alpha output buffer)
@@ -94,17 +97,36 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
         T.state[u] = 0;
 }
 
-// Scaled cost of one cell from the point clouds: -sum_k (rs x_ik - rs y_jk)^2,
-// accumulated in coordinate order (the points sweep computes the same bits).
-__device__ __forceinline__ float cl_points(const TiledArgs &T, int b, int i, int j) {
-    const float *x = T.X + ((size_t)b * T.d1 + i) * T.D;
-    const float *y = T.Y + ((size_t)b * T.d2 + j) * T.D;
+// Scaled cost of one cell from the point clouds, in the centred expansion
+// form every kernel uses: with x' = rs (x_i - c), y' = rs (y_j - c),
+//   cl_ij = fma(2x'_0, y'_0, fma(2x'_1, y'_1, ... fma(2x'_{D-1}, y'_{D-1}, -|y'|^2))) - |x'|^2.
+// Centring keeps the three terms of the size of the clouds' spread, so the
+// rounding error stays that of the distance itself.
+template <int DM>
+__device__ __forceinline__ void centred(const float *p, const float *c, float rs, int D, float (&o)[DM]) {
+#pragma unroll
+    for (int k = 0; k < DM; ++k) o[k] = k < D ? rs * (p[k] - c[k]) : 0.f;
+}
+template <int DM>
+__device__ __forceinline__ float sqnorm(const float (&o)[DM]) {
     float acc = 0.f;
-    for (int k = 0; k < T.D; ++k) {
-        const float dd = T.rs * x[k] - T.rs * y[k];
-        acc = __builtin_fmaf(dd, dd, acc);
-    }
-    return -acc;
+#pragma unroll
+    for (int k = 0; k < DM; ++k) acc = __builtin_fmaf(o[k], o[k], acc);
+    return acc;
+}
+template <int DM>
+__device__ __forceinline__ float dot2_from(const float (&x)[DM], const float (&y)[DM], float init) {
+    float acc = init;
+#pragma unroll
+    for (int k = DM - 1; k >= 0; --k) acc = __builtin_fmaf(2.f * x[k], y[k], acc);
+    return acc;
+}
+__device__ __forceinline__ float cl_points(const TiledArgs &T, int b, int i, int j) {
+    float x[kPointsMaxD], y[kPointsMaxD];
+    const float *c = T.ctr + (size_t)b * 4;
+    centred(T.X + ((size_t)b * T.d1 + i) * T.D, c, T.rs, T.D, x);
+    centred(T.Y + ((size_t)b * T.d2 + j) * T.D, c, T.rs, T.D, y);
+    return dot2_from(x, y, -sqnorm(y)) - sqnorm(x);
 }
 __device__ __forceinline__ float cl_at(const TiledArgs &T, const float *Cb, int b, int i, int j) {
     return T.X ? cl_points(T, b, i, j) : -T.s * Cb[(size_t)i * T.d2 + j];
@@ -347,32 +369,113 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
     }
 }
 
-// Cost of the lane's columns from point coordinates held in registers: the
-// row's scaled coordinates xs against the columns' ys (padding columns sit
-// at kFarCoord: cl = -3e36, plan entry 0, 0 * cl finite).
-constexpr float kFarCoord = 1.0e18f;
-template <int NCW, int D>
-struct PointsCost {
-    const float (&ys)[NCW][D];
-    const float (&xs)[D];
-    __device__ __forceinline__ float operator()(int c) const {
+// Mean point of each problem's two clouds (fixed-order sums): the centre of
+// the expansion form above.  One work-group per problem.
+__global__ __launch_bounds__(kThreads) void sk_tiled_center(TiledArgs T) {
+    __shared__ float red[kWaves];
+    const int b = blockIdx.x;
+    for (int k = 0; k < T.D; ++k) {
         float acc = 0.f;
-#pragma unroll
-        for (int k = 0; k < D; ++k) {
-            const float dd = xs[k] - ys[c][k];
-            acc = __builtin_fmaf(dd, dd, acc);
-        }
-        return -acc;
+        for (int i = threadIdx.x; i < T.d1; i += kThreads) acc += T.X[((size_t)b * T.d1 + i) * T.D + k];
+        for (int j = threadIdx.x; j < T.d2; j += kThreads) acc += T.Y[((size_t)b * T.d2 + j) * T.D + k];
+        acc = block_sum(acc, red);
+        if (threadIdx.x == 0) T.ctr[(size_t)b * 4 + k] = acc / (float)(T.d1 + T.d2);
     }
+}
+
+// Padding columns sit at kFarCoord: |y'|^2 = 3e36, the plan entry is 0 and
+// the cost finite (0 * cl = 0).
+constexpr float kFarCoord = 1.0e18f;
+
+// RB rows of a point-cloud problem in one wavefront (the structure of
+// row_step, with the rows' reductions interleaved so their latencies
+// overlap): u_c = b_j + cl_ij + |x'_i|^2 = fma chain of 2x'.y' on
+// bp_c = b_j - |y'_j|^2, so a cell costs three fmas, one add and the exp2.
+// Row q takes part only if live[q] (wavefront-uniform).
+template <int NCW, int D, int RB, bool STATS>
+__device__ __forceinline__ void rows_step_points(const float (&ys)[NCW][D], const float (&bp)[NCW],
+                                                 const float (&xc)[RB][D], const float (&ai)[RB],
+                                                 const float (&mui)[RB], const bool (&live)[RB], float *const (&a_row)[RB],
+                                                 float (&colpart)[NCW], float &rowerr, float &losspart, int lane) {
+    float xx[RB], e[RB][NCW], rs[RB];
+#pragma unroll
+    for (int q = 0; q < RB; ++q) {
+        xx[q] = sqnorm(xc[q]);
+        const float ax = ai[q] - xx[q];
+#pragma unroll
+        for (int c = 0; c < NCW; ++c) e[q][c] = live[q] ? ex2(dot2_from(xc[q], ys[c], bp[c]) + ax) : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < RB; ++q) rs[q] = wave_sum(tree_sum<NCW>(e[q]));
+    if (STATS) {
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+#pragma unroll
+            for (int c = 0; c < NCW; ++c) {
+                const float cl = dot2_from(xc[q], ys[c], -sqnorm(ys[c])) - xx[q];
+                losspart = __builtin_fmaf(e[q][c], cl, losspart);
+                colpart[c] += e[q][c];
+            }
+            if (live[q] && mui[q] > 0.f) rowerr += fabsf(rs[q] - mui[q]);
+        }
+        return;
+    }
+    float f[RB];
+#pragma unroll
+    for (int q = 0; q < RB; ++q) {
+        f[q] = 0.f;  // zero-mass or idle row: a_i = -inf, all its entries 0
+        if (!live[q] || !(mui[q] > 0.f)) continue;
+        const float lmu = log2f(mui[q]);
+        float an;
+        if (rs[q] >= kSumLo && rs[q] <= kSumHi) {
+            an = ai[q] + lmu - lg2(rs[q]);
+            f[q] = ex2(an - ai[q]);
+            rowerr += fabsf(f[q] * rs[q] - mui[q]);
+        } else {
+            // Exact u-update (max, then sum) over b_j + cl_ij = u_c - |x'|^2
+            // (u_c recomputed in each pass: this path is rare and keeps
+            // no extra registers).
+            float m = neg_inf();
+#pragma unroll
+            for (int c = 0; c < NCW; ++c) m = fmaxf(m, dot2_from(xc[q], ys[c], bp[c]));
+            m = wave_max(m);
+            float s2 = 0.f;
+#pragma unroll
+            for (int c = 0; c < NCW; ++c) s2 += ex2(dot2_from(xc[q], ys[c], bp[c]) - m);
+            s2 = wave_sum(s2);
+            an = lmu - ((m - xx[q]) + lg2(s2));
+            const float ax2 = an - xx[q];
+#pragma unroll
+            for (int c = 0; c < NCW; ++c) e[q][c] = ex2(dot2_from(xc[q], ys[c], bp[c]) + ax2);
+            f[q] = 1.f;
+            rowerr += fabsf(wave_sum(tree_sum<NCW>(e[q])) - mui[q]);
+        }
+        if (lane == 0) *a_row[q] = an;
+    }
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        float acc = colpart[c];
+#pragma unroll
+        for (int q = 0; q < RB; ++q) acc = __builtin_fmaf(e[q][c], f[q], acc);
+        colpart[c] = acc;
+    }
+}
+
+// Rows reduced together by the points sweep (their plan entries stay in
+// registers until the row sums are known).
+template <int NCW>
+struct PointsShape {
+    static constexpr int RB = NCW <= 8 ? 4 : (NCW <= 16 ? 2 : 1);
 };
 
 // Sweep over per-sample point clouds (the on-the-fly cost of Section 4's
 // closing remark: cost entries are recreated from the points, no cost matrix
 // exists).  Work-group (row block r, problem b) as in sk_tiled_sweep; lane l
-// keeps the scaled coordinates of its columns j = l + 64 c in registers.  The
-// row's coordinates, potential and mass are loaded one row ahead through a
-// lane-varying index, so they arrive in vector registers (vector operands
-// taken from scalar registers issue at half rate on this chip).
+// keeps the centred, scaled coordinates of its columns j = l + 64 c in
+// registers.  The row's coordinates, potential and mass are loaded one row
+// ahead through a lane-varying index, so they arrive in vector registers
+// (vector operands taken from scalar registers issue at half rate on this
+// chip).
 template <int NCW, int D, bool STATS>
 __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, int k) {
     extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
@@ -396,37 +499,66 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, i
     const float *xb = T.X + (size_t)b * d1 * D;
     const float *yb = T.Y + (size_t)b * d2 * D;
     const float rs = T.rs;
+    float cen[D];  // the centre, in registers (a memory operand would be re-read after every store)
+#pragma unroll
+    for (int q = 0; q < D; ++q) cen[q] = T.ctr[(size_t)b * 4 + q];
 
-    float bv[NCW], colpart[NCW], ys[NCW][D];
+    // The columns' raw coordinates first (clamped index: all loads in
+    // flight together), then centred and scaled; padding columns go far away.
+    float bp[NCW], colpart[NCW], ys[NCW][D];
 #pragma unroll
     for (int c = 0; c < NCW; ++c) {
-        const int j = lane + 64 * c;
-        bv[c] = bsrc[j];  // 0 past d2 (padded stride)
-        colpart[c] = 0.f;
+        const int jj = min(lane + 64 * c, d2 - 1);
 #pragma unroll
-        for (int q = 0; q < D; ++q) ys[c][q] = j < d2 ? rs * yb[(size_t)j * D + q] : kFarCoord;
+        for (int q = 0; q < D; ++q) ys[c][q] = yb[(size_t)jj * D + q];
+        bp[c] = bsrc[lane + 64 * c];  // 0 past d2 (padded stride)
     }
+#pragma unroll
+    for (int c = 0; c < NCW; ++c) {
+        const bool in = lane + 64 * c < d2;
+#pragma unroll
+        for (int q = 0; q < D; ++q) ys[c][q] = in ? rs * (ys[c][q] - cen[q]) : kFarCoord;
+        bp[c] -= sqnorm(ys[c]);
+        colpart[c] = 0.f;
+    }
+    // Rows i0 + w + kWaves t, RB at a time; the next batch's coordinates,
+    // potentials and masses are loaded one batch ahead.
+    constexpr int RB = PointsShape<NCW>::RB;
     int vz = 0;
     __asm__ volatile("" : "+v"(vz));  // a zero the compiler cannot see as uniform
-    float xn[D], an = 0.f, mn = 0.f;
-    auto load_row = [&](int i) {
-        const int ii = i + vz;
+    float xn[RB][D], an[RB], mn[RB];
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    // Raw values only: the arithmetic on them waits for the next batch, so
+    // the loads stay in flight over this batch's work.
+    auto load_rows = [&](int i) {
 #pragma unroll
-        for (int q = 0; q < D; ++q) xn[q] = rs * xb[(size_t)ii * D + q];
-        an = ab[ii];
-        mn = mub[ii];
+        for (int q = 0; q < RB; ++q) {
+            const int ii = min(i + q * kWaves, i1 - 1) + vz;  // an idle slot re-reads the last row
+#pragma unroll
+            for (int d = 0; d < D; ++d) xn[q][d] = xb[(size_t)ii * D + d];
+            an[q] = ab[ii];
+            mn[q] = mub[ii];
+        }
     };
     float rowerr = 0.f, losspart = 0.f;
-    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
-    if (i0 + w < i1) load_row(i0 + w);
-    for (int i = i0 + w; i < i1; i += kWaves) {
-        float xs[D];
+    if (i0 + w < i1) load_rows(i0 + w);
+    for (int i = i0 + w; i < i1; i += RB * kWaves) {
+        float xc[RB][D], ai[RB], mui[RB];
+        bool live[RB];
+        float *arow[RB];
 #pragma unroll
-        for (int q = 0; q < D; ++q) xs[q] = xn[q];
-        const float ai = an, mui = mn;
-        if (i + kWaves < i1) load_row(i + kWaves);  // another row of this wavefront: no conflict with the store below
-        const PointsCost<NCW, D> cost{ys, xs};
-        row_step<NCW, STATS>(cost, ai, mui, ab + i, bv, colpart, rowerr, losspart, lane);
+        for (int q = 0; q < RB; ++q) {
+#pragma unroll
+            for (int d = 0; d < D; ++d) xc[q][d] = rs * (xn[q][d] - cen[d]);
+            ai[q] = an[q];
+            mui[q] = mn[q];
+            live[q] = i + q * kWaves < i1;
+            arow[q] = ab + min(i + q * kWaves, i1 - 1);
+        }
+        // Other rows of this wavefront (no conflict with the stores below);
+        // unconditional, clamped to the last row, so the waits stay exact.
+        load_rows(i + RB * kWaves);
+        rows_step_points<NCW, D, RB, STATS>(ys, bp, xc, ai, mui, live, arow, colpart, rowerr, losspart, lane);
     }
 
     // Combine the wavefronts' partials in LDS, fixed order, and store.
@@ -1142,7 +1274,7 @@ void row_blocks(int B, int d1, int d2, int kind, int *R, int *RBS) {
 }
 
 struct Layout {
-    size_t bbuf, part, rowerr, lossp, colerr, state, a2, total;
+    size_t bbuf, part, rowerr, lossp, colerr, state, a2, ctr, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1188,6 +1320,8 @@ Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC
     off = align256(off + sizeof(int32_t) * (size_t)B);
     L.a2 = off;
     if (stream_shape(d2, kind)) off = align256(off + sizeof(float) * (size_t)B * d1);
+    L.ctr = off;
+    if (kind == kKindPoints) off = align256(off + sizeof(float) * 4 * (size_t)B);
     L.total = off;
     if (R_out) *R_out = R;
     if (RBS_out) *RBS_out = RBS;
@@ -1284,6 +1418,7 @@ template <int NCW, int D>
 hipError_t run_points(const TiledArgs &T, hipStream_t st) {
     const size_t lds = sizeof(float) * kWaves * NCW * 64;
     const dim3 grid(T.R, T.B), blk(kThreads);
+    hipLaunchKernelGGL(sk_tiled_center, dim3(T.B), blk, 0, st, T);
     return run_sequence(
         T, st, [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_points<NCW, D, false>), grid, blk, lds, st, T, k); },
         [&]() { hipLaunchKernelGGL((sk_tiled_sweep_points<NCW, D, true>), grid, blk, lds, st, T, 0); });
@@ -1353,6 +1488,7 @@ TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     T.C = a.C;
     T.X = nullptr;
     T.Y = nullptr;
+    T.ctr = nullptr;
     T.D = 0;
     T.rs = 0.f;
     T.a = a.alpha;
@@ -1390,6 +1526,7 @@ hipError_t launch_tiled_points(const FwdArgs &a, const float *X, const float *Y,
     T.C = nullptr;
     T.X = X;
     T.Y = Y;
+    T.ctr = reinterpret_cast<float *>(static_cast<char *>(ws) + L.ctr);
     T.D = D;
     T.rs = (float)rs;
     const int ncw = (a.d2 + 63) / 64;
