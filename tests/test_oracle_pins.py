@@ -524,3 +524,84 @@ def test_fd_gradient_points():
 def test_points_grads_planted_mistakes_are_caught(mutation):
     ok, _, _ = _points_grads_fd_case(mutation)
     assert not ok
+
+
+# --------------------------------------------------------------------------
+# Gradient of the sharp loss E^0 (implicit differentiation of the plan)
+# --------------------------------------------------------------------------
+
+def _E0(mu, nu, C, lam):
+    o = _converged(mu, nu, C, lam)
+    return o["loss"][0], o
+
+
+@pytest.mark.parametrize("lam", [0.05, 0.3])
+def test_fd_sharp_gradient(lam):
+    """d E^0 along mean-zero moves e_i - e_k of mu (and of nu), by central
+    differences of the converged E^0 = <P, C>, matches <grad, e> from the
+    implicit-differentiation solve; it differs from the multiplier gradient by
+    O(lambda) (Section 5: the multiplier gradient is that of E^lambda)."""
+    rng = np.random.default_rng(31)
+    d1, d2 = 6, 5
+    mu, nu = _rand_hist(rng, d1), _rand_hist(rng, d2)
+    C = rng.uniform(0, 1, (d1, d2))
+    _, o = _E0(mu, nu, C, lam)
+    gs = oracle.sharp_gradient([1.0], mu, nu, C, lam, o["alpha"], o["beta"])
+    gm = oracle.backward([1.0], mu, nu, C, lam, o["alpha"], o["beta"])
+    h = 1e-6
+    for (i, k) in [(0, 3), (2, 5), (4, 1)]:
+        e = np.zeros(d1); e[i], e[k] = 1.0, -1.0
+        fd = (_E0(mu + h * e, nu, C, lam)[0] - _E0(mu - h * e, nu, C, lam)[0]) / (2 * h)
+        assert fd == pytest.approx(gs["grad_mu"][0] @ e, abs=1e-7, rel=1e-5)
+    for (j, k) in [(0, 4), (3, 1)]:
+        e = np.zeros(d2); e[j], e[k] = 1.0, -1.0
+        fd = (_E0(mu, nu + h * e, C, lam)[0] - _E0(mu, nu - h * e, C, lam)[0]) / (2 * h)
+        assert fd == pytest.approx(gs["grad_nu"][0] @ e, abs=1e-7, rel=1e-5)
+    # the two gradients differ (the multiplier one is that of E^lambda, not E^0)
+    assert np.abs(gs["grad_mu"] - gm["grad_mu"]).max() > 1e-4
+
+
+def test_sharp_gradient_zero_mass_and_batch():
+    """Zero masses get gradient 0 and leave the support's system unchanged;
+    each problem of a batch is independent; grad_loss scales each problem."""
+    rng = np.random.default_rng(33)
+    d1, d2, lam = 6, 7, 0.1
+    mu = np.stack([_rand_hist(rng, d1) for _ in range(2)])
+    nu = np.stack([_rand_hist(rng, d2) for _ in range(2)])
+    mu[1, 2] = 0.0; mu[1] /= mu[1].sum()
+    C = rng.uniform(0, 1, (d1, d2))
+    o = oracle.forward(mu, nu, C, lam, 3000)
+    g = oracle.sharp_gradient([2.0, 0.5], mu, nu, C, lam, o["alpha"], o["beta"])
+    assert g["grad_mu"][1, 2] == 0.0
+    one = oracle.sharp_gradient([1.0], mu[1:], nu[1:], C, lam, o["alpha"][1:], o["beta"][1:])
+    np.testing.assert_allclose(g["grad_mu"][1], 0.5 * one["grad_mu"][0], rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(g["grad_mu"][1, [0, 1, 3, 4, 5]].sum(), 0.0, atol=1e-12)
+
+
+@pytest.mark.parametrize("mutation", ["no_coupling", "lambda_factor", "multiplier_rhs"])
+def test_sharp_gradient_planted_mistakes_are_caught(mutation):
+    """Plausible mistakes in the implicit-differentiation system (dropping the
+    plan coupling, a stray lambda, the marginals instead of the cost-weighted
+    sums on the right-hand side) disagree with the finite differences that
+    pin the oracle."""
+    rng = np.random.default_rng(34)
+    d1, d2, lam = 5, 6, 0.1
+    mu, nu = _rand_hist(rng, d1), _rand_hist(rng, d2)
+    C = rng.uniform(0, 1, (d1, d2))
+    _, o = _E0(mu, nu, C, lam)
+    P = oracle.plan(C, lam, o["alpha"][0], o["beta"][0])
+    H = np.block([[np.diag(P.sum(1)), P], [P.T, np.diag(P.sum(0))]])
+    rhs = np.concatenate([(P * C).sum(1), (P * C).sum(0)])
+    if mutation == "no_coupling":
+        H = np.diag(np.diag(H))
+    elif mutation == "lambda_factor":
+        rhs = lam * rhs
+    elif mutation == "multiplier_rhs":
+        rhs = np.concatenate([P.sum(1), P.sum(0)])
+    z = np.linalg.lstsq(H, rhs, rcond=None)[0][:d1]
+    e = np.zeros(d1); e[1], e[3] = 1.0, -1.0
+    h = 1e-6
+    fd = (_E0(mu + h * e, nu, C, lam)[0] - _E0(mu - h * e, nu, C, lam)[0]) / (2 * h)
+    good = oracle.sharp_gradient([1.0], mu, nu, C, lam, o["alpha"], o["beta"])["grad_mu"][0] @ e
+    assert fd == pytest.approx(good, rel=1e-5, abs=1e-7)
+    assert abs((z - z.mean()) @ e - fd) > 1e-4, mutation
