@@ -138,6 +138,29 @@ SK_API sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss,
                             void *stream);
 
 /*
+ * Gradient of the sharp loss E^0 = sum_ij P_ij C_ij itself with respect to
+ * (mu, nu) (Section 5 points to this sharper gradient; sinkhorn_backward
+ * returns the multiplier gradient of E^lambda).  The plan P of (alpha, beta)
+ * is differentiated through its marginal constraints: with r = P 1,
+ * c = P^T 1, a = (P o C) 1, b = (P o C)^T 1 the gradient is the solution z of
+ *     [diag(r)  P      ] z = (a, b),
+ *     [P^T      diag(c)]
+ * each block centred over the support of mu (resp. nu) and 0 off it, times
+ * grad_loss[b].  The matrix is singular along (1, -1); the right-hand side is
+ * projected off that direction.  Solved per problem by conjugate gradients
+ * preconditioned with (r, c): at most max_cg (>= 1) iterations, stopping when
+ * the preconditioned residual norm falls below cg_tol (>= 0) times its start
+ * value.  Shapes: max(d1, d2) <= 128 (SK_ERR_SHAPE otherwise).  cg_iters
+ * [B] int32 (may be NULL) receives the iterations taken.  Needs no
+ * workspace; deterministic.  Invalid max_cg or cg_tol: SK_ERR_ITERS.
+ */
+SK_API sk_status sinkhorn_backward_sharp(const sk_problem *p, const float *grad_loss,
+                                  const float *mu, const float *nu, const float *C,
+                                  const float *alpha, const float *beta, float *grad_mu,
+                                  float *grad_nu, int32_t max_cg, float cg_tol,
+                                  int32_t *cg_iters, void *stream);
+
+/*
  * Point clouds.  The cost is the squared Euclidean distance between points,
  *     C_ij = sum_k (X[i,k] - Y[j,k])^2,   k < D,   1 <= D <= 16,
  * with X [d1, D] and Y [d2, D] shared by the batch (c_batched = 0) or

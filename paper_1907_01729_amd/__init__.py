@@ -15,6 +15,7 @@ from ._binding import (  # noqa: F401
     load_library,
     sinkhorn_backward,
     sinkhorn_backward_points,
+    sinkhorn_backward_sharp,
     sinkhorn_forward,
     sinkhorn_forward_points,
     sinkhorn_points_workspace_bytes,
@@ -32,6 +33,7 @@ __all__ = [
     "load_library",
     "sinkhorn_backward",
     "sinkhorn_backward_points",
+    "sinkhorn_backward_sharp",
     "sinkhorn_forward",
     "sinkhorn_forward_points",
     "sinkhorn_loss",

@@ -29,6 +29,7 @@ EXPORTED = (
     "sinkhorn_points_workspace_bytes",
     "sinkhorn_forward_points",
     "sinkhorn_backward_points",
+    "sinkhorn_backward_sharp",
 )
 
 
@@ -83,6 +84,8 @@ def load_library():
     lib.sinkhorn_forward_points.restype = ctypes.c_int
     lib.sinkhorn_backward_points.argtypes = [PP, I, P, P, P, P, P, P, P, P, P, P, P, P]
     lib.sinkhorn_backward_points.restype = ctypes.c_int
+    lib.sinkhorn_backward_sharp.argtypes = [PP, P, P, P, P, P, P, P, P, I, ctypes.c_float, P, P]
+    lib.sinkhorn_backward_sharp.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -262,3 +265,24 @@ def sinkhorn_backward_points(grad_loss, mu, nu, X, Y, lam, alpha, beta, grad_poi
         out["grad_X"] = gX
         out["grad_Y"] = gY
     return out
+
+
+def sinkhorn_backward_sharp(grad_loss, mu, nu, C, lam, alpha, beta, max_cg=200, cg_tol=1e-6, stream=None):
+    """Gradient of the sharp loss E^0 itself (implicit differentiation of the
+    plan, conjugate gradients per problem): dict(grad_mu, grad_nu, cg_iters)."""
+    lib = load_library()
+    for t, n in ((grad_loss, "grad_loss"), (mu, "mu"), (nu, "nu"), (C, "C"), (alpha, "alpha"), (beta, "beta")):
+        _dev(t, n)
+    B, d1, d2, cb = _shapes(mu, nu, C)
+    p = problem(B, d1, d2, cb, lam, 0, 0.0)
+    dev = mu.device
+    f = dict(device=dev, dtype=torch.float32)
+    gmu = torch.empty((B, d1), **f)
+    gnu = torch.empty((B, d2), **f)
+    its = torch.empty((B,), device=dev, dtype=torch.int32)
+    st = lib.sinkhorn_backward_sharp(ctypes.byref(p), _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
+                                     _ptr(beta), _ptr(gmu), _ptr(gnu), int(max_cg), ctypes.c_float(cg_tol),
+                                     _ptr(its), _stream(dev, stream))
+    if st != 0:
+        raise SinkhornError(st, "sinkhorn_backward_sharp")
+    return dict(grad_mu=gmu, grad_nu=gnu, cg_iters=its)

@@ -200,6 +200,35 @@ sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const f
     return e == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 
+sk_status sinkhorn_backward_sharp(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu,
+                                  const float *C, const float *alpha, const float *beta, float *grad_mu,
+                                  float *grad_nu, int32_t max_cg, float cg_tol, int32_t *cg_iters, void *stream) {
+    sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (p->d1 > sk::kSharpMaxD || p->d2 > sk::kSharpMaxD) return SK_ERR_SHAPE;
+    if (max_cg < 1 || !(cg_tol >= 0.f) || !isfinite(cg_tol)) return SK_ERR_ITERS;
+    if (p->B == 0) return SK_OK;
+    if (!grad_loss || !mu || !nu || !C || !alpha || !beta || !grad_mu || !grad_nu) return SK_ERR_NULLPTR;
+    sk::SharpArgs a;
+    a.grad_loss = grad_loss;
+    a.mu = mu;
+    a.nu = nu;
+    a.C = C;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.grad_mu = grad_mu;
+    a.grad_nu = grad_nu;
+    a.cg_iters = cg_iters;
+    a.B = p->B;
+    a.d1 = p->d1;
+    a.d2 = p->d2;
+    a.c_batched = p->c_batched;
+    a.max_cg = max_cg;
+    a.s = sk::kLog2eHost / p->lambda;
+    a.cg_tol = cg_tol;
+    return sk::launch_sharp(a, static_cast<hipStream_t>(stream)) == hipSuccess ? SK_OK : SK_ERR_HIP;
+}
+
 sk_status sinkhorn_forward_points(const sk_problem *p, int32_t D, const float *mu, const float *nu, const float *X,
                                   const float *Y, float *alpha, float *beta, float *loss, float *marg_err,
                                   int32_t *iters, void *workspace, size_t ws_bytes, void *stream) {

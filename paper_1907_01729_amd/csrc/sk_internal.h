@@ -57,6 +57,19 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);
 
 hipError_t launch_backward(const BwdArgs &a, hipStream_t st);
 
+// Gradient of the sharp loss E^0 (implicit differentiation of the plan,
+// conjugate gradients per problem); the plan of one problem sits in LDS.
+constexpr int kSharpMaxD = 128;
+struct SharpArgs {
+    const float *grad_loss, *mu, *nu, *C, *alpha, *beta;
+    float *grad_mu, *grad_nu;
+    int32_t *cg_iters;  // may be null
+    int B, d1, d2, c_batched, max_cg;
+    float s;  // log2(e) / lambda
+    float cg_tol;
+};
+hipError_t launch_sharp(const SharpArgs &a, hipStream_t st);
+
 // Point clouds (C_ij = sum_k (x_ik - y_jk)^2).  The tiled sweep computes the
 // cost on the fly for per-sample clouds with up to kPointsMaxD coordinates
 // and d2 <= kPointsMaxD2 (the columns' coordinates live in registers); other

@@ -1,0 +1,166 @@
+// sk_sharp.hip -- gradient of the sharp loss E^0 = <P, C> with respect to
+// (mu, nu) (Section 5 points to this sharper gradient; the multiplier
+// gradient of sk_backward.hip is that of E^lambda).
+//
+// Implicit differentiation of the entropic plan through its marginal
+// constraints: a change of the marginals moves the plan by
+// dP_ij = P_ij (df_i + dg_j) / lambda with
+//     [diag(r)  P      ] [df]            [dmu]
+//     [P^T      diag(c)] [dg] = lambda * [dnu],       r = P 1, c = P^T 1,
+// and dE^0 = (<a, df> + <b, dg>) / lambda with a = (P o C) 1, b = (P o C)^T 1,
+// so the gradient is the solution z of H z = (a, b) for the same symmetric
+// matrix H.  H is positive semi-definite and singular along (1, -1) (a
+// constant moved from f to g); the right-hand side is projected off that
+// direction and each block of z is centred over its support afterwards
+// (the gradient on the simplex is defined up to a constant per block; 0 off
+// the support).  Solved per problem by conjugate gradients preconditioned
+// with diag(H) = (r, c).
+//
+// One work-group of 256 threads per problem, max(d1, d2) <= 128: P lives in
+// LDS with an odd row stride (conflict-free both along rows and along
+// columns); thread t < 128 owns row t, thread 128 + t owns column t, so one
+// pass over P forms both halves of H p.  Reductions are fixed-order block
+// sums (deterministic).
+#include "sk_device.h"
+#include "sk_internal.h"
+
+namespace sk {
+namespace {
+
+constexpr int kShThreads = 256;
+constexpr int kShHalf = kShThreads / 2;  // rows on threads [0, 128), columns on [128, 256)
+static_assert(kShHalf >= kSharpMaxD, "one thread per row and per column");
+
+__device__ __forceinline__ float block_sum(float v, float *red) {
+    v = wave_sum(v);
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    __syncthreads();
+    if (lane == 0) red[w] = v;
+    __syncthreads();
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < kShThreads / 64; ++k) s += red[k];
+    return s;
+}
+
+__host__ __device__ __forceinline__ int ld_of(int d2) { return d2 | 1; }  // odd row stride
+
+__global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
+    extern __shared__ float P[];  // [d1][ld]
+    __shared__ float pv[2 * kShHalf];
+    __shared__ float red[kShThreads / 64];
+    const int b = blockIdx.x, t = threadIdx.x;
+    const int d1 = A.d1, d2 = A.d2, ld = ld_of(d2);
+    const float *Cb = A.C + (A.c_batched ? (size_t)b * d1 * d2 : 0);
+    const float *al = A.alpha + (size_t)b * d1;
+    const float *be = A.beta + (size_t)b * d2;
+
+    // The plan of (alpha, beta), base 2: P_ij = 2^(a_i + b_j - s C_ij).
+    for (int u = t; u < d1 * d2; u += kShThreads) {
+        const int i = u / d2, j = u - i * d2;
+        P[i * ld + j] = ex2(__builtin_fmaf(be[j], kLog2e, al[i] * kLog2e) - A.s * Cb[u]);
+    }
+    __syncthreads();
+
+    const bool isrow = t < kShHalf;
+    const int k = isrow ? t : t - kShHalf;
+    const bool own = isrow ? k < d1 : k < d2;
+    // Diagonal of H (the plan's marginal) and the right-hand side (a or b).
+    float dg = 0.f, rhs = 0.f;
+    if (own) {
+        if (isrow) {
+            for (int j = 0; j < d2; ++j) {
+                const float p = P[k * ld + j];
+                dg += p;
+                rhs = __builtin_fmaf(p, Cb[(size_t)k * d2 + j], rhs);
+            }
+        } else {
+            for (int i = 0; i < d1; ++i) {
+                const float p = P[i * ld + k];
+                dg += p;
+                rhs = __builtin_fmaf(p, Cb[(size_t)i * d2 + k], rhs);
+            }
+        }
+    }
+    const float mass = own ? (isrow ? A.mu[(size_t)b * d1 + k] : A.nu[(size_t)b * d2 + k]) : 0.f;
+    const bool sup = own && mass > 0.f && dg > 0.f;
+    if (!sup) {
+        dg = 0.f;
+        rhs = 0.f;
+    }
+    // Project the right-hand side off (1, -1) over the supports.
+    {
+        const float sgn = isrow ? 1.f : -1.f;
+        const float dot = block_sum(sup ? sgn * rhs : 0.f, red);
+        const float n = block_sum(sup ? 1.f : 0.f, red);
+        if (sup) rhs -= sgn * (dot / n);
+    }
+
+    // Jacobi-preconditioned conjugate gradients; every scalar below is a
+    // block sum, so the control flow is uniform across the work-group.
+    float x = 0.f, r = rhs;
+    float z = sup ? r / dg : 0.f, p = z;
+    float rz = block_sum(r * z, red);
+    const float stop = A.cg_tol * A.cg_tol * rz;
+    int it = 0;
+    if (rz > 0.f) {
+        while (it < A.max_cg) {
+            if (own) pv[isrow ? k : kShHalf + k] = p;
+            __syncthreads();
+            float q = dg * p;
+            if (sup) {
+                if (isrow) {
+                    for (int j = 0; j < d2; ++j) q = __builtin_fmaf(P[k * ld + j], pv[kShHalf + j], q);
+                } else {
+                    for (int i = 0; i < d1; ++i) q = __builtin_fmaf(P[i * ld + k], pv[i], q);
+                }
+            }
+            const float pq = block_sum(p * q, red);  // its barriers also retire the reads of pv
+            if (!(pq > 0.f)) break;
+            const float step = rz / pq;
+            x = __builtin_fmaf(step, p, x);
+            r = __builtin_fmaf(-step, q, r);
+            z = sup ? r / dg : 0.f;
+            const float rzn = block_sum(r * z, red);
+            ++it;
+            if (!(rzn > stop)) break;
+            p = __builtin_fmaf(rzn / rz, p, z);
+            rz = rzn;
+        }
+    }
+
+    // Centre each block over its support, scale by the upstream gradient.
+    const float sx_r = block_sum(sup && isrow ? x : 0.f, red);
+    const float n_r = block_sum(sup && isrow ? 1.f : 0.f, red);
+    const float sx_c = block_sum(sup && !isrow ? x : 0.f, red);
+    const float n_c = block_sum(sup && !isrow ? 1.f : 0.f, red);
+    const float g = A.grad_loss[b];
+    if (own) {
+        const float mean = isrow ? (n_r > 0.f ? sx_r / n_r : 0.f) : (n_c > 0.f ? sx_c / n_c : 0.f);
+        const float v = sup ? g * (x - mean) : 0.f;
+        if (isrow)
+            A.grad_mu[(size_t)b * d1 + k] = v;
+        else
+            A.grad_nu[(size_t)b * d2 + k] = v;
+    }
+    if (t == 0 && A.cg_iters) A.cg_iters[b] = it;
+}
+
+size_t sharp_lds_bytes(int d1, int d2) { return sizeof(float) * (size_t)d1 * ld_of(d2); }
+
+}  // namespace
+
+hipError_t launch_sharp(const SharpArgs &a, hipStream_t st) {
+    const size_t lds = sharp_lds_bytes(a.d1, a.d2);
+    static bool attr = false;  // above 64 KB of LDS (d near 128) needs the larger dynamic limit
+    if (!attr) {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_sharp_kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)sharp_lds_bytes(kSharpMaxD, kSharpMaxD));
+        attr = true;
+    }
+    hipLaunchKernelGGL(sk_sharp_kernel, dim3(a.B), dim3(kShThreads), lds, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace sk

@@ -142,3 +142,18 @@ def test_points_workspace_sizes():
     assert sk.sinkhorn_points_workspace_bytes(32, 1024, 2100, 1, 3, 0.05, 100) >= 32 * 1024 * 2100 * 4
     shared = sk.sinkhorn_points_workspace_bytes(32, 784, 784, 0, 2, 0.01, 100)
     assert shared >= 784 * 784 * 4 + sk.sinkhorn_workspace_bytes(32, 784, 784, 0, 0.01, 100)
+
+
+def test_sharp_rejections_on_host():
+    lib = sk.load_library()
+    v = None
+
+    def call(p, max_cg=10, tol=1e-6):
+        return lib.sinkhorn_backward_sharp(ctypes.byref(p), v, v, v, v, v, v, v, v, max_cg, ctypes.c_float(tol),
+                                           None, None)
+    assert call(_binding.problem(4, 129, 10, 0, 0.1, 0)) == -2
+    assert call(_binding.problem(4, 10, 10, 0, 0.0, 0)) == -3
+    assert call(_binding.problem(4, 10, 10, 0, 0.1, 0), max_cg=0) == -4
+    assert call(_binding.problem(4, 10, 10, 0, 0.1, 0), tol=float("nan")) == -4
+    assert call(_binding.problem(4, 10, 10, 0, 0.1, 0)) == -1
+    assert call(_binding.problem(0, 10, 10, 0, 0.1, 0)) == 0
