@@ -91,18 +91,23 @@ def stored_traffic(profile_name, src_hash):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(prob, grad_C):
+def cpu_baseline(prob, grad_C, sharp=False):
     """The fp64 oracle, as it stands, on the host cores: the same step
     (forward + backward) on the whole batch."""
     import oracle
 
     t0 = time.perf_counter()
     o = oracle.forward(prob.mu, prob.nu, prob.C, prob.lam, prob.n_iter, tol=prob.tol)
-    oracle.backward(np.ones(prob.B), prob.mu, prob.nu, prob.C, prob.lam, o["alpha"], o["beta"], grad_C=grad_C)
+    if sharp:
+        oracle.sharp_gradient(np.ones(prob.B), prob.mu, prob.nu, prob.C, prob.lam, o["alpha"], o["beta"])
+    else:
+        oracle.backward(np.ones(prob.B), prob.mu, prob.nu, prob.C, prob.lam, o["alpha"], o["beta"],
+                        grad_C=grad_C)
     dt = time.perf_counter() - t0
     cells = float(np.sum(o["iters"].astype(np.float64))) * prob.d1 * prob.d2
     return dict(value=cells / dt, unit="cell-updates/s", cores=oracle.num_threads(), kind="oracle",
-                sample=f"whole batch of workload {prob.name} (B={prob.B}), one forward+backward, {dt:.2f} s")
+                sample=f"whole batch of workload {prob.name} (B={prob.B}), one forward+backward"
+                       f"{' (gradient of E^0, dense solve)' if sharp else ''}, {dt:.2f} s")
 
 
 def cpu_baseline_sampled(prob, grad_C, n_samples):
@@ -144,6 +149,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sharp", action="store_true",
+                    help="backward = gradient of E^0 itself (implicit differentiation, conjugate gradients; "
+                         "resident shapes: configs 1 and 2)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 3 times (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -168,6 +176,9 @@ def main():
     import workloads
 
     points = args.config == 6
+    if args.sharp and args.config not in (1, 2):
+        print("bench.py: --sharp takes configs 1 and 2 (max(d1, d2) <= 128)", file=sys.stderr)
+        sys.exit(2)
     prob = workloads.clouds_points() if points else workloads.make_config(args.config)
     grad_C = bool(prob.grad_points) if points else bool(prob.grad_C)
     dev = torch.device("cuda:0")
@@ -196,6 +207,8 @@ def main():
             return sk.sinkhorn_forward(mu, nu, C, prob.lam, n, prob.tol, workspace=ws)
 
         def bwd(out):
+            if args.sharp:
+                return sk.sinkhorn_backward_sharp(g, mu, nu, C, prob.lam, out["alpha"], out["beta"])
             return sk.sinkhorn_backward(g, mu, nu, C, prob.lam, out["alpha"], out["beta"], grad_C=grad_C)
     regime = sk.sinkhorn_regime(prob.B, prob.d1, prob.d2, int(prob.c_batched), prob.lam, prob.n_iter, prob.tol)
 
@@ -212,6 +225,7 @@ def main():
 
     stream = torch.cuda.current_stream(dev)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    bev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     e_all0, e_all1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -220,12 +234,15 @@ def main():
         ev[k][0].record(stream)
         out = fwd(prob.n_iter)
         ev[k][1].record(stream)
+        bev[k][0].record(stream)
         bwd(out)
+        bev[k][1].record(stream)
     e_all1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = e_all0.elapsed_time(e_all1) / args.steps
     fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    bwd_ms = float(np.mean([a.elapsed_time(b) for a, b in bev]))
 
     # Roofline of the dominant kernel.
     if regime == 1:
@@ -313,6 +330,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
         "wall_ms_per_step": wall / args.steps * 1e3,
+        "fwd_ms": fwd_ms,
+        "bwd_ms": bwd_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -323,6 +342,8 @@ def main():
             "B": prob.B, "d1": prob.d1, "d2": prob.d2, "lambda": prob.lam, "n_iter": prob.n_iter,
             "tol": prob.tol, "c_batched": bool(prob.c_batched), "iters_done_mean": float(iters.mean()),
             **({"D": prob.D, "cost": "from points"} if points else {}),
+            **({"backward": "sharp: gradient of E^0 by implicit differentiation (conjugate gradients)"}
+               if args.sharp else {}),
             "regime": {1: "resident", 2: "tiled"}.get(regime, "?"),
         },
         "roofline": roof,
@@ -331,7 +352,7 @@ def main():
         if points:
             res["cpu_baseline"] = cpu_baseline_points(prob, 2)
         elif args.config in (1, 2):
-            res["cpu_baseline"] = cpu_baseline(prob, grad_C)
+            res["cpu_baseline"] = cpu_baseline(prob, grad_C, sharp=args.sharp)
         else:
             res["cpu_baseline"] = cpu_baseline_sampled(prob, grad_C, {3: 16, 4: 1, 5: 2}[args.config])
     print(json.dumps(res), flush=True)

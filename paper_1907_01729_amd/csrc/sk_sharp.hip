@@ -45,9 +45,35 @@ __device__ __forceinline__ float block_sum(float v, float *red) {
 
 __host__ __device__ __forceinline__ int ld_of(int d2) { return d2 | 1; }  // odd row stride
 
+// sum_m a[m * stride] * v[m], m < n, from LDS: eight loads in flight and four
+// independent accumulators (a single chain would wait on every load).
+__device__ __forceinline__ float dot_lds(const float *a, int stride, const float *v, int n) {
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    int m = 0;
+    for (; m + 8 <= n; m += 8) {
+        float x[8], y[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            x[u] = a[(m + u) * stride];
+            y[u] = v[m + u];
+        }
+        s0 = __builtin_fmaf(x[0], y[0], s0);
+        s1 = __builtin_fmaf(x[1], y[1], s1);
+        s2 = __builtin_fmaf(x[2], y[2], s2);
+        s3 = __builtin_fmaf(x[3], y[3], s3);
+        s0 = __builtin_fmaf(x[4], y[4], s0);
+        s1 = __builtin_fmaf(x[5], y[5], s1);
+        s2 = __builtin_fmaf(x[6], y[6], s2);
+        s3 = __builtin_fmaf(x[7], y[7], s3);
+    }
+    for (; m < n; ++m) s0 = __builtin_fmaf(a[m * stride], v[m], s0);
+    return (s0 + s1) + (s2 + s3);
+}
+
 __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
-    extern __shared__ float P[];  // [d1][ld]
+    extern __shared__ float P[];  // [d1][ld]: the cost first, then the plan
     __shared__ float pv[2 * kShHalf];
+    __shared__ float av[kShHalf], bw[kShHalf];  // base-2 potentials
     __shared__ float red[kShThreads / 64];
     const int b = blockIdx.x, t = threadIdx.x;
     const int d1 = A.d1, d2 = A.d2, ld = ld_of(d2);
@@ -55,33 +81,46 @@ __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
     const float *al = A.alpha + (size_t)b * d1;
     const float *be = A.beta + (size_t)b * d2;
 
-    // The plan of (alpha, beta), base 2: P_ij = 2^(a_i + b_j - s C_ij).
+    // Stage the cost (coalesced) and the potentials in LDS.
+    if (t < d1) av[t] = al[t] * kLog2e;
+    if (t < d2) bw[t] = be[t] * kLog2e;
     for (int u = t; u < d1 * d2; u += kShThreads) {
         const int i = u / d2, j = u - i * d2;
-        P[i * ld + j] = ex2(__builtin_fmaf(be[j], kLog2e, al[i] * kLog2e) - A.s * Cb[u]);
+        P[i * ld + j] = Cb[u];
     }
     __syncthreads();
 
     const bool isrow = t < kShHalf;
     const int k = isrow ? t : t - kShHalf;
     const bool own = isrow ? k < d1 : k < d2;
-    // Diagonal of H (the plan's marginal) and the right-hand side (a or b).
+    // Diagonal of H (the plan's marginal) and the right-hand side (a or b),
+    // with the plan entries P_ij = 2^(a_i + b_j - s C_ij) formed on the way.
     float dg = 0.f, rhs = 0.f;
     if (own) {
         if (isrow) {
+            const float a = av[k];
             for (int j = 0; j < d2; ++j) {
-                const float p = P[k * ld + j];
+                const float c = P[k * ld + j];
+                const float p = ex2((a + bw[j]) - A.s * c);
                 dg += p;
-                rhs = __builtin_fmaf(p, Cb[(size_t)k * d2 + j], rhs);
+                rhs = __builtin_fmaf(p, c, rhs);
             }
         } else {
+            const float bb = bw[k];
             for (int i = 0; i < d1; ++i) {
-                const float p = P[i * ld + k];
+                const float c = P[i * ld + k];
+                const float p = ex2((av[i] + bb) - A.s * c);
                 dg += p;
-                rhs = __builtin_fmaf(p, Cb[(size_t)i * d2 + k], rhs);
+                rhs = __builtin_fmaf(p, c, rhs);
             }
         }
     }
+    __syncthreads();  // the cost has been read: the plan overwrites it
+    for (int u = t; u < d1 * d2; u += kShThreads) {
+        const int i = u / d2, j = u - i * d2;
+        P[i * ld + j] = ex2((av[i] + bw[j]) - A.s * P[i * ld + j]);
+    }
+    __syncthreads();
     const float mass = own ? (isrow ? A.mu[(size_t)b * d1 + k] : A.nu[(size_t)b * d2 + k]) : 0.f;
     const bool sup = own && mass > 0.f && dg > 0.f;
     if (!sup) {
@@ -108,13 +147,7 @@ __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
             if (own) pv[isrow ? k : kShHalf + k] = p;
             __syncthreads();
             float q = dg * p;
-            if (sup) {
-                if (isrow) {
-                    for (int j = 0; j < d2; ++j) q = __builtin_fmaf(P[k * ld + j], pv[kShHalf + j], q);
-                } else {
-                    for (int i = 0; i < d1; ++i) q = __builtin_fmaf(P[i * ld + k], pv[i], q);
-                }
-            }
+            if (sup) q += isrow ? dot_lds(P + k * ld, 1, pv + kShHalf, d2) : dot_lds(P + k, ld, pv, d1);
             const float pq = block_sum(p * q, red);  // its barriers also retire the reads of pv
             if (!(pq > 0.f)) break;
             const float step = rz / pq;
