@@ -149,6 +149,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the workload's batch size (same generator); the line then names the override")
+    ap.add_argument("--tol", type=float, default=None,
+                    help="override the workload's early-stop tolerance on the marginal L1 error")
     ap.add_argument("--sharp", action="store_true",
                     help="backward = gradient of E^0 itself (implicit differentiation, conjugate gradients; "
                          "resident shapes: configs 1 and 2)")
@@ -179,7 +183,10 @@ def main():
     if args.sharp and args.config not in (1, 2):
         print("bench.py: --sharp takes configs 1 and 2 (max(d1, d2) <= 128)", file=sys.stderr)
         sys.exit(2)
-    prob = workloads.clouds_points() if points else workloads.make_config(args.config)
+    over = {"B": args.batch} if args.batch else {}
+    prob = workloads.clouds_points(**over) if points else workloads.make_config(args.config, **over)
+    if args.tol is not None:
+        prob.tol = args.tol
     grad_C = bool(prob.grad_points) if points else bool(prob.grad_C)
     dev = torch.device("cuda:0")
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
@@ -344,6 +351,8 @@ def main():
             **({"D": prob.D, "cost": "from points"} if points else {}),
             **({"backward": "sharp: gradient of E^0 by implicit differentiation (conjugate gradients)"}
                if args.sharp else {}),
+            **({"overrides": {k: v for k, v in (("B", args.batch or None), ("tol", args.tol)) if v is not None}}
+               if (args.batch or args.tol is not None) else {}),
             "regime": {1: "resident", 2: "tiled"}.get(regime, "?"),
         },
         "roofline": roof,

@@ -26,6 +26,9 @@
 // the same decision, and the first row block records K = k in the stop flag,
 // which later sweeps and merges honour.  Row-error partials are double
 // buffered so a decision never reads a partial being rewritten.
+#include <stdlib.h>
+#include <string.h>
+
 #include "sk_device.h"
 #include "sk_internal.h"
 
@@ -56,6 +59,10 @@ struct TiledArgs {
     float *lossp;    // [R][B] loss partials (stats)
     float *colerr;   // [B][JC] column-error partials of the merge
     int32_t *state;  // [B] 0 = running, K > 0 = stopped after iteration K
+    // Compaction of the shared-cost sweep's batch (early stop only; else
+    // null): order[0, nlive) lists the running problems in increasing order,
+    // rebuilt by sk_tiled_compact before every sweep k >= 2.
+    int32_t *order, *nlive;
     float *alpha_out, *beta_out, *loss_out, *merr_out;
     int32_t *iters_out;
     int B, d1, d2, R, RBS, JC, n_iter, c_batched;
@@ -589,6 +596,49 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, i
     }
 }
 
+// Early-stop decision and compaction before sweep k (k >= 2, tol > 0) of the
+// shared-cost sweep: every running problem whose iterate k-1 met tol is
+// stopped (the same fixed-order test the sweeps otherwise take), and the
+// running ones are listed in increasing order, so that the sweep's
+// work-groups take only running problems (W per group) and whole groups of
+// stopped problems are never scheduled.  One work-group; a block-wide
+// prefix sum per 1024 problems keeps the order deterministic.
+constexpr int kCompactThreads = 1024;
+__global__ __launch_bounds__(kCompactThreads) void sk_tiled_compact(TiledArgs T, int k) {
+    __shared__ int wsum[kCompactThreads / 64];
+    __shared__ int base;
+    if (threadIdx.x == 0) base = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    for (int b0 = 0; b0 < T.B; b0 += kCompactThreads) {
+        const int b = b0 + threadIdx.x;
+        bool live = false;
+        if (b < T.B && T.state[b] == 0) {
+            if (stop_before(T, b, k))
+                T.state[b] = k - 1;
+            else
+                live = true;
+        }
+        // exclusive prefix sum of the live flags: within the wavefront by
+        // ballot, across wavefronts through LDS
+        const unsigned long long m = __ballot(live);
+        const int before = __popcll(m & ((1ull << lane) - 1ull));
+        if (lane == 0) wsum[w] = __popcll(m);
+        __syncthreads();
+        int off = base;
+        for (int q = 0; q < w; ++q) off += wsum[q];
+        if (live) T.order[off + before] = b;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int tot = 0;
+            for (int q = 0; q < kCompactThreads / 64; ++q) tot += wsum[q];
+            base += tot;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *T.nlive = base;
+}
+
 typedef float f4v __attribute__((ext_vector_type(4)));
 
 // Sweep for a cost shared by the batch (Section 4's setting).
@@ -675,13 +725,18 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     // everything derived from it (problem, staging assignments) is scalar.
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int d1 = T.d1, d2 = T.d2;
-    const int b_raw = g * W + w;
+    // Problem of this wavefront: slot g W + w of the running list when the
+    // batch is compacted (the stop test already taken), else problem g W + w.
+    const bool compacted = !STATS && T.order && k >= 2;
+    const int slot = g * W + w;
+    const int nslot = compacted ? __builtin_amdgcn_readfirstlane(*T.nlive) : T.B;
+    const int b_raw = slot < nslot ? (compacted ? __builtin_amdgcn_readfirstlane(T.order[slot]) : slot) : T.B;
     // Inactive wavefronts (past the batch, or stopped) keep staging and
     // reaching the barriers; they compute nothing and store nothing.
     const int b = b_raw < T.B ? b_raw : T.B - 1;
     bool skip = b_raw >= T.B;
     const int st = T.state[b];
-    if (!STATS && !skip) {
+    if (!STATS && !skip && !compacted) {
         if (st != 0) {
             skip = true;
         } else if (stop_before(T, b, k)) {
@@ -1274,7 +1329,7 @@ void row_blocks(int B, int d1, int d2, int kind, int *R, int *RBS) {
 }
 
 struct Layout {
-    size_t bbuf, part, rowerr, lossp, colerr, state, a2, ctr, total;
+    size_t bbuf, part, rowerr, lossp, colerr, state, order, a2, ctr, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1318,6 +1373,8 @@ Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC
     off = align256(off + sizeof(float) * (size_t)B * JC);
     L.state = off;
     off = align256(off + sizeof(int32_t) * (size_t)B);
+    L.order = off;  // order[B] then nlive
+    if (kind == kKindShared) off = align256(off + sizeof(int32_t) * ((size_t)B + 1));
     L.a2 = off;
     if (stream_shape(d2, kind)) off = align256(off + sizeof(float) * (size_t)B * d1);
     L.ctr = off;
@@ -1409,6 +1466,7 @@ hipError_t run_shared(const TiledArgs &T, hipStream_t st) {
     return run_sequence(
         T, st,
         [&](int k) {
+            if (T.order && k >= 2) hipLaunchKernelGGL(sk_tiled_compact, dim3(1), dim3(kCompactThreads), 0, st, T, k);
             hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>), grid, blk, lds, st, T, k);
         },
         [&]() { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>), grid, blk, lds, st, T, 0); });
@@ -1499,6 +1557,8 @@ TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     T.lossp = reinterpret_cast<float *>(base + L.lossp);
     T.colerr = reinterpret_cast<float *>(base + L.colerr);
     T.state = reinterpret_cast<int32_t *>(base + L.state);
+    T.order = nullptr;
+    T.nlive = nullptr;
     T.alpha_out = a.alpha;
     T.beta_out = a.beta;
     T.loss_out = a.loss;
@@ -1545,6 +1605,13 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     const int W = shared_width(a.B, a.c_batched);
     // 16-byte global->LDS copies need 16-byte aligned cost rows.
     const bool vec4 = a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0;
+    // Early stop with W problems per work-group: compact the running
+    // problems before each sweep (diagnostic switch SK_TILED_COMPACT=0 off).
+    const char *cenv = getenv("SK_TILED_COMPACT");
+    if (W && a.tol > 0.f && !(cenv && !strcmp(cenv, "0"))) {
+        T.order = reinterpret_cast<int32_t *>(base + L.order);
+        T.nlive = T.order + a.B;
+    }
     if (W == 8) return vec4 ? dispatch_shared<8, true>(T, ncw, st) : dispatch_shared<8, false>(T, ncw, st);
     if (W == 4) return vec4 ? dispatch_shared<4, true>(T, ncw, st) : dispatch_shared<4, false>(T, ncw, st);
     if (stream_shape(a.d2, a.c_batched ? kKindBatched : kKindShared) && ((uintptr_t)a.C % 16) == 0) {

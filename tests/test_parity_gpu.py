@@ -500,3 +500,22 @@ def test_stream_small_lambda_exact_paths():
                                     cost="grid1d")
     gpu, ref = check_forward(prob, merr_atol=1e-4)
     check_backward(prob, gpu, ref)
+
+
+# ---------------------------------------------------------------- early stop with batch compaction (shared sweep)
+
+def test_shared_sweep_early_stop_compaction(monkeypatch):
+    """Image histograms with an early stop: problems stop at different
+    iterations; the shared-cost sweep compacts the running problems into its
+    8-problem work-groups.  Parity with the oracle at the GPU's iteration
+    counts, and the same bits as without compaction."""
+    prob = workloads.make_config(3, B=24, side=20, n_iter=400)
+    prob.tol = 2e-4
+    monkeypatch.setenv("SK_TILED_COMPACT", "0")
+    plain = _gpu(prob)
+    monkeypatch.delenv("SK_TILED_COMPACT")
+    gpu, ref = check_forward(prob)
+    its = gpu["iters"]
+    assert (its < prob.n_iter).sum() >= prob.B - 2 and len(set(its.tolist())) > 3, its
+    for k in plain:
+        np.testing.assert_array_equal(gpu[k], plain[k])
