@@ -25,9 +25,10 @@
 // The kernel verifies the symmetry of the cost first, pair by pair (bit
 // equality); a cost that is not symmetric marks every problem with iters = -2
 // for the matrix-core kernel, launched next.  A problem outside the plain
-// form's range gets iters = -1 (the log-domain kernel takes it), at the start
-// or as soon as a guard fails: a sum R_i, S_j outside [2^-64, 2^64] or a
-// scaling U_i, V_j outside [2^-100, 2^100] on the supports.
+// form's range gets iters = -1 (the log-domain kernel takes it): a cost
+// spread wider than the range at the start, or a guard that failed in any
+// iteration (checked once, at the end): a sum R_i, S_j outside
+// [2^-64, 2^64] or a scaling U_i, V_j outside [2^-100, 2^100] on the supports.
 #include "sk_device.h"
 #include "sk_internal.h"
 
@@ -161,10 +162,11 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     constexpr int XS = 20;
     static_assert(2 * H <= XS, "row blocks per column-block line");
     __shared__ __attribute__((aligned(16))) float xs[2][8 * XS];  // xs[0] = U, xs[1] = V
-    // Per-wavefront reports: [iteration parity][phase][wavefront][error, failure].
+    // Per-wavefront error reports of the stop test: [iteration parity]
+    // [wavefront][row phase, column phase], one 16-byte read per decision.
     // The parity keeps a report readable until both wavefronts have passed
     // the next iteration's barriers.
-    __shared__ float red[2][2][2][2];
+    __shared__ __attribute__((aligned(16))) float red[2][2][2];
     __shared__ float ini[2][2][4];  // set-up exchanges
 
     const int lane = threadIdx.x & 63;
@@ -292,84 +294,84 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
 #pragma unroll
         for (int t = NC & ~3; t < NC; ++t) wc[t] = line[t];
     };
+    // A scaling out of range (or a sum that would push one there) marks the
+    // problem for the log-domain kernel.  The mark is kept per lane and
+    // exchanged once, after the loop: iterating on after a failure costs
+    // time but cannot trap, and a failed problem's outputs are never written.
+    bool bad_acc = false;
+
     // v-update of iteration 1.
     gather_lds(xs[0]);
     kmul<H, NC>(K, wc, X, q);
     {
         const float v = ns * __builtin_amdgcn_rcpf(X[0]);
-        const bool bad = (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+        bad_acc |= (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
         V = ns > 0.f ? v : 0.f;
         if (own) xs[1][xl] = V;
-        const float fb = __any(bad) ? 1.f : 0.f;
-        if (lane == 0) red[0][1][w][1] = fb;
     }
     __syncthreads();
-    bool fail = red[0][1][0][1] + red[0][1][1][1] != 0.f;
+    gather_lds(xs[1]);
 
     // Iteration k: R = K V and the u-update; then (k < n_iter) S = K^T U = K U,
-    // the stop test of iterate k (its row error from the u-update, its column
-    // error from S and the V it was built with) and the v-update of k+1.
-    for (int k = 1; !fail && k <= n_iter; ++k) {
-        float(&rd)[2][2][2] = red[k & 1];
-        gather_lds(xs[1]);
+    // the v-update of k+1 and the stop test of iterate k (its row error from
+    // the u-update, its column error from S and the V it was built with).
+    // The next product's operand is read before that test, which only
+    // discards it.
+    for (int k = 1; k <= n_iter; ++k) {
+        float(&rd)[2][2] = red[k & 1];
         kmul<H, NC>(K, wc, X, q);
         {
             const float u = ms * __builtin_amdgcn_rcpf(X[0]);
-            const bool bad = (ms > 0.f) & !(sum_ok(X[0]) & scale_ok(u));
+            bad_acc |= (ms > 0.f) & !(sum_ok(X[0]) & scale_ok(u));
             U = ms > 0.f ? u : 0.f;
             if (own) xs[0][xl] = U;
-            const float e = check ? wave_sum(ms > 0.f ? fabsf(u * X[0] - ms) : 0.f) : 0.f;
-            const float fb = __any(bad) ? 1.f : 0.f;
-            if (lane == 0) {
-                rd[0][w][0] = e;
-                rd[0][w][1] = fb;
+            if (check) {
+                const float e = wave_sum(ms > 0.f ? fabsf(u * X[0] - ms) : 0.f);
+                if (lane == 0) rd[w][0] = e;
             }
         }
         __syncthreads();
-        if (k == n_iter) {
-            fail = rd[0][0][1] + rd[0][1][1] != 0.f;
-            break;
-        }
+        if (k == n_iter) break;
 
-        // (A failed u-update is acted on after the next barrier: the product
-        // in between only spends time.)
         gather_lds(xs[0]);
         kmul<H, NC>(K, wc, X, q);
         {
-            const float e = check ? wave_sum(ns > 0.f ? fabsf(V * X[0] - ns) : 0.f) : 0.f;
             const float v = ns * __builtin_amdgcn_rcpf(X[0]);
-            const bool bad = (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+            bad_acc |= (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+            if (check) {
+                const float e = wave_sum(ns > 0.f ? fabsf(V * X[0] - ns) : 0.f);
+                if (lane == 0) rd[w][1] = e;
+            }
             Vold = V;
             V = ns > 0.f ? v : 0.f;
             if (own) xs[1][xl] = V;
-            const float fb = __any(bad) ? 1.f : 0.f;
-            if (lane == 0) {
-                rd[1][w][0] = e;
-                rd[1][w][1] = fb;
-            }
         }
         __syncthreads();
-        if (rd[0][0][1] + rd[0][1][1] != 0.f) {  // the u-update of iterate k failed
-            fail = true;
-            break;
+        gather_lds(xs[1]);
+        if (check) {
+            const float4 e4 = *reinterpret_cast<const float4 *>(&rd[0][0]);
+            if ((e4.x + e4.y) + (e4.z + e4.w) <= tol) {
+                kstop = k;  // the returned plan is iterate k: U and the V it was built with
+                V = Vold;
+                break;
+            }
         }
-        if (check && (rd[0][0][0] + rd[0][1][0]) + (rd[1][0][0] + rd[1][1][0]) <= tol) {
-            kstop = k;  // the returned plan is iterate k: U and the V it was built with
-            V = Vold;
-            break;
-        }
-        fail = rd[1][0][1] + rd[1][1][1] != 0.f;
     }
-    if (fail) {
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+    {
+        const float fb = __any(bad_acc) ? 1.f : 0.f;
+        if (lane == 0) ini[0][w][0] = fb;
     }
 
     // ---- the returned plan P = U K V, measured (Section 4): its marginals
-    // and sum_ij P_ij C_ij from the cost itself.  No wavefront reads the
-    // operand buffers between the loop's last barrier and here. ----
+    // and sum_ij P_ij C_ij from the cost itself.  Past the loop's last
+    // barrier a wavefront reads the operand buffers only for a gather whose
+    // values it drops (a stop), so rewriting V here is safe. ----
     if (own) xs[1][xl] = V;
     __syncthreads();
+    if (ini[0][0][0] + ini[0][1][0] != 0.f) {
+        if (threadIdx.x == 0) A.iters[b] = -1;
+        return;
+    }
     gather_lds(xs[1]);
     kmul<H, NC>(K, wc, X, q);  // row sums R = K V
     float err = ms > 0.f ? fabsf(U * X[0] - ms) : 0.f, lsum;
@@ -394,8 +396,8 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     err = wave_sum(err);
     lsum = wave_sum(lsum);
     if (lane == 0) {
-        red[0][0][w][0] = err;
-        red[0][0][w][1] = lsum;
+        red[0][w][0] = err;
+        red[0][w][1] = lsum;
     }
     if (own && x < d) {
         A.alpha[(size_t)b * d + x] = kLn2 * lg2(U);
@@ -403,8 +405,8 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        A.loss[b] = red[0][0][0][1] + red[0][0][1][1];
-        A.marg_err[b] = red[0][0][0][0] + red[0][0][1][0];
+        A.loss[b] = red[0][0][1] + red[0][1][1];
+        A.marg_err[b] = red[0][0][0] + red[0][1][0];
         A.iters[b] = kstop;
     }
 }

@@ -312,6 +312,27 @@ def test_sym_kernel_hands_over_out_of_range(monkeypatch):
     check_forward(prob, merr_atol=1e-4)
 
 
+@pytest.mark.parametrize("tol,n_iter", [(0.0, 50), (1e-5, 300)])
+def test_sym_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
+    """A positive but tiny mass (1e-37) puts its row scaling below 2^-100 in
+    the first u-update, a guard the symmetric kernel checks inside the
+    iteration (the cost spread itself is in range): alone it returns that
+    problem unsolved (iters = -1) and the rest solved; with the fallback the
+    problem matches the oracle and the others keep their bits."""
+    prob = workloads.random_problem(seed=35, B=6, d1=70, d2=70, lam=0.1, n_iter=n_iter, cost="sym", tol=tol)
+    prob.mu[2, 5] = 1e-37
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    alone = _gpu(prob)
+    rest = np.arange(prob.B) != 2
+    assert alone["iters"][2] == -1
+    assert np.all(alone["iters"][rest] >= 1)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref)
+    for k in ("alpha", "beta", "loss", "marg_err", "iters"):
+        np.testing.assert_array_equal(gpu[k][rest], alone[k][rest])
+
+
 def test_sym_kernel_early_stop(monkeypatch):
     prob = workloads.random_problem(seed=34, B=8, d1=80, d2=80, lam=0.1, n_iter=400, tol=1e-5, cost="sym")
     out = {}
