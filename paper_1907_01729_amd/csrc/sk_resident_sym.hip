@@ -13,11 +13,10 @@
 // for its row blocks r in [w H, w H + H) and every column block t < NC
 // (8 NC >= d, H = ceil(NC / 2)).  A product K w takes w "by columns"
 // (register t of lane (p, q) holds w[q + 8t], read from LDS), forms per-lane
-// partial row sums over t, and reduces them over the 8 lanes q (lane bits 5,
-// 4, 3) by a reduce-scatter: at each step a lane keeps half of its rows and
-// adds its partner's copy of the same rows (v_permlane32_swap,
-// v_permlane16_swap, then DPP row_ror:8), so that each row total ends in one
-// lane.  The update runs on that lane only and publishes the new scaling to
+// partial row sums over t, and sums them over the 8 lanes q through a small
+// per-wavefront LDS transpose: lane (p, q) writes its H partials, lane
+// (p, r) reads the 8 partials of its row r and adds them, so that each row
+// total ends in one lane.  The update runs on that lane only and publishes the new scaling to
 // LDS for the next product; one barrier per product.  Because K is symmetric,
 // K^T U is the same product as K U, so one register copy of K serves both
 // passes.
@@ -44,85 +43,31 @@ constexpr float kRangeBits = 64.f;
 __device__ __forceinline__ bool sum_ok(float x) { return x >= kLo && x <= kHi; }
 __device__ __forceinline__ bool scale_ok(float x) { return x >= kSMin && x <= kSMax; }
 
-// ---- reduce-scatter bookkeeping (compile time) ----
-// A step over N entries: the low lane keeps entries [0, H), the high lane
-// [H, N), H = ceil(N / 2); a step over a single entry is an all-reduce (both
-// lanes keep it, the low lane owns it).
-constexpr int half_up(int n) { return (n + 1) / 2; }
-template <int NC>
-struct Scatter {
-    static constexpr int N1 = half_up(NC), N2 = half_up(N1), S = half_up(N2);  // S: slots per lane
-};
-
-// Row index r (rows p + 8r) held by slot s of the lanes with column block q
-// (lane bits 5, 4, 3 = q bits 2, 1, 0), or -1 when the slot holds no row of
-// its own (padding or a duplicate).
-constexpr int scatter_row(int NC, int q, int s) {
-    int n = NC, base = 0, cnt = NC;
-    const int bits[3] = {(q >> 2) & 1, (q >> 1) & 1, q & 1};
-    for (int k = 0; k < 3; ++k) {
-        if (n == 1) {
-            if (bits[k]) return -1;
-            continue;
-        }
-        const int h = half_up(n);
-        if (bits[k]) {
-            base += h;
-            cnt = cnt > h ? cnt - h : 0;
-        } else {
-            cnt = cnt < h ? cnt : h;
-        }
-        n = h;
-    }
-    return s < cnt ? base + s : -1;
-}
-
-// One reduce-scatter step over lane bit BIT (5, 4 or 3).
-template <int BIT, int N>
-__device__ __forceinline__ void scatter_step(const float (&v)[N], float (&w)[half_up(N)], bool hi) {
-    constexpr int H = half_up(N);
-    if constexpr (N == 1) {
-        if constexpr (BIT == 5) {
-            const LanePair x = swap32(v[0]);
-            w[0] = x.lo + x.hi;
-        } else if constexpr (BIT == 4) {
-            const LanePair x = swap16(v[0]);
-            w[0] = x.lo + x.hi;
-        } else {
-            w[0] = v[0] + dpp<kRowRor8>(v[0]);
-        }
-    } else {
+// Row totals through LDS: lane (p, q) holds partial sums x[r] of rows
+// p + 8 (r0 + r) over its column blocks; lane (p, r), r < NR, gets the total
+// of its row r, summed over q in a fixed order (other lanes get a copy of
+// row NR - 1).  tb is the wavefront's own scratch of 8 x 72 floats, entry
+// (p, r, q) at p * 72 + r * 8 + q: the 64 writes of one r fall on 64
+// distinct banks and each total is two 16-byte reads.  The LDS operations of
+// one wavefront complete in order, so no barrier is needed, and the next
+// call's writes cannot overtake this call's reads.
+template <int NR>
+__device__ __forceinline__ float row_totals(const float (&x)[NR], float *tb, int p, int q) {
+    static_assert(NR <= 8, "one row per lane q");
+    float *mine = tb + p * 72 + q;
 #pragma unroll
-        for (int m = 0; m < H; ++m) {
-            const float a = v[m], b = H + m < N ? v[H + m] : v[m];
-            if constexpr (BIT == 3) {
-                // Within a DPP row (partner lane ^ 8): keep one, send the other.
-                w[m] = (hi ? b : a) + dpp<kRowRor8>(hi ? a : b);
-            } else {
-                // The swap leaves (a, partner's a) on the low lanes and
-                // (partner's b, b) on the high lanes: one add completes either.
-                const auto x = BIT == 5
-                                   ? __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false)
-                                   : __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-                w[m] = __uint_as_float(x[0]) + __uint_as_float(x[1]);
-            }
-        }
-    }
+    for (int r = 0; r < NR; ++r) mine[r * 8] = x[r];
+    __builtin_amdgcn_wave_barrier();
+    const float *row = tb + p * 72 + (q < NR ? q : NR - 1) * 8;
+    const float4 a = *reinterpret_cast<const float4 *>(row);
+    const float4 b = *reinterpret_cast<const float4 *>(row + 4);
+    __builtin_amdgcn_wave_barrier();
+    return ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w));
 }
 
-template <int NC>
-__device__ __forceinline__ void scatter(const float (&x)[NC], float (&out)[Scatter<NC>::S], int q) {
-    using SC = Scatter<NC>;
-    float x1[SC::N1], x2[SC::N2];
-    scatter_step<5, NC>(x, x1, (q & 4) != 0);
-    scatter_step<4, SC::N1>(x1, x2, (q & 2) != 0);
-    scatter_step<3, SC::N2>(x2, out, (q & 1) != 0);
-}
-
-// out = K w for the column-layout w, in the slot layout (NR row blocks).
+// (K w) of the lane's row for the column-layout w (NR row blocks).
 template <int NR, int NC>
-__device__ __forceinline__ void kmul(const float (&K)[NR][NC], const float (&wc)[NC], float (&out)[Scatter<NR>::S],
-                                     int q) {
+__device__ __forceinline__ float kmul(const float (&K)[NR][NC], const float (&wc)[NC], float *tb, int p, int q) {
     float x[NR];
 #pragma unroll
     for (int r = 0; r < NR; ++r) x[r] = K[r][0] * wc[0];
@@ -130,7 +75,7 @@ __device__ __forceinline__ void kmul(const float (&K)[NR][NC], const float (&wc)
     for (int t = 1; t < NC; ++t)
 #pragma unroll
         for (int r = 0; r < NR; ++r) x[r] = __builtin_fmaf(K[r][t], wc[t], x[r]);
-    scatter<NR>(x, out, q);
+    return row_totals<NR>(x, tb, p, q);
 }
 
 // Buffer descriptor over the cost from row 8r on (reads past the end of the
@@ -154,8 +99,6 @@ __device__ __forceinline__ float load_cell(__amdgpu_buffer_rsrc_t rsrc, int byte
 template <int NC>
 __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     constexpr int H = (NC + 1) / 2;
-    constexpr int S = Scatter<H>::S;
-    static_assert(S == 1, "one slot per lane");
     // Column operand in LDS, by column block: row y at [y & 7][y >> 3], so
     // that lane (p, q) reads its NC values contiguously (16-byte reads; a
     // stride of 20 floats puts the 8 blocks q on distinct banks).
@@ -168,6 +111,7 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     // the next iteration's barriers.
     __shared__ __attribute__((aligned(16))) float red[2][2][2];
     __shared__ float ini[2][2][4];  // set-up exchanges
+    __shared__ __attribute__((aligned(16))) float tsum[2][8 * 72];  // per-wavefront row-total scratch
 
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: descriptors stay scalar
@@ -247,16 +191,12 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
 #pragma unroll
         for (int t = 0; t < NC; ++t) K[i][t] = ex2(fminf(-s * K[i][t] - clmax, 0.f));
 
-    // The lane's slot: row x = p + 8 (r0 + rr) of its wavefront, or none
-    // (own = false: a duplicate after an all-reduce step).  Marginals are 0
-    // off the problem.
-    int rr = -1;
-#pragma unroll
-    for (int qq = 0; qq < 8; ++qq)
-        if (q == qq) rr = scatter_row(H, qq, 0);
-    const bool own = rr >= 0;
-    const int x = own ? p + 8 * (r0 + rr) : 0;
-    const int xl = p * XS + r0 + rr;  // its place in the LDS operand
+    // The lane's row: x = p + 8 (r0 + q) for q < H (the row whose total the
+    // lane receives), none for the other lanes.  Marginals are 0 off the
+    // problem.
+    const bool own = q < H;
+    const int x = own ? p + 8 * (r0 + q) : 0;
+    const int xl = p * XS + r0 + q;  // its place in the LDS operand
     const float ms = own && x < d ? A.mu[(size_t)b * d + x] : 0.f;
     const float ns = own && x < d ? A.nu[(size_t)b * d + x] : 0.f;
     {
@@ -278,7 +218,8 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     const float tol = A.tol;
     const bool check = tol > 0.f;
     int kstop = n_iter;
-    float U = 0.f, V, Vold = 0.f, X[S], wc[NC];
+    float U = 0.f, V, Vold = 0.f, X, wc[NC];
+    float *const tb = tsum[w];
 
     // Column layout from LDS: register t of lane (p, q) takes row q + 8t.
     auto gather_lds = [&](const float *src) {
@@ -302,10 +243,10 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
 
     // v-update of iteration 1.
     gather_lds(xs[0]);
-    kmul<H, NC>(K, wc, X, q);
+    X = kmul<H, NC>(K, wc, tb, p, q);
     {
-        const float v = ns * __builtin_amdgcn_rcpf(X[0]);
-        bad_acc |= (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+        const float v = ns * __builtin_amdgcn_rcpf(X);
+        bad_acc |= (ns > 0.f) & !(sum_ok(X) & scale_ok(v));
         V = ns > 0.f ? v : 0.f;
         if (own) xs[1][xl] = V;
     }
@@ -319,14 +260,14 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     // discards it.
     for (int k = 1; k <= n_iter; ++k) {
         float(&rd)[2][2] = red[k & 1];
-        kmul<H, NC>(K, wc, X, q);
+        X = kmul<H, NC>(K, wc, tb, p, q);
         {
-            const float u = ms * __builtin_amdgcn_rcpf(X[0]);
-            bad_acc |= (ms > 0.f) & !(sum_ok(X[0]) & scale_ok(u));
+            const float u = ms * __builtin_amdgcn_rcpf(X);
+            bad_acc |= (ms > 0.f) & !(sum_ok(X) & scale_ok(u));
             U = ms > 0.f ? u : 0.f;
             if (own) xs[0][xl] = U;
             if (check) {
-                const float e = wave_sum(ms > 0.f ? fabsf(u * X[0] - ms) : 0.f);
+                const float e = wave_sum(ms > 0.f ? fabsf(u * X - ms) : 0.f);
                 if (lane == 0) rd[w][0] = e;
             }
         }
@@ -334,12 +275,12 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
         if (k == n_iter) break;
 
         gather_lds(xs[0]);
-        kmul<H, NC>(K, wc, X, q);
+        X = kmul<H, NC>(K, wc, tb, p, q);
         {
-            const float v = ns * __builtin_amdgcn_rcpf(X[0]);
-            bad_acc |= (ns > 0.f) & !(sum_ok(X[0]) & scale_ok(v));
+            const float v = ns * __builtin_amdgcn_rcpf(X);
+            bad_acc |= (ns > 0.f) & !(sum_ok(X) & scale_ok(v));
             if (check) {
-                const float e = wave_sum(ns > 0.f ? fabsf(V * X[0] - ns) : 0.f);
+                const float e = wave_sum(ns > 0.f ? fabsf(V * X - ns) : 0.f);
                 if (lane == 0) rd[w][1] = e;
             }
             Vold = V;
@@ -373,12 +314,12 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
         return;
     }
     gather_lds(xs[1]);
-    kmul<H, NC>(K, wc, X, q);  // row sums R = K V
-    float err = ms > 0.f ? fabsf(U * X[0] - ms) : 0.f, lsum;
+    X = kmul<H, NC>(K, wc, tb, p, q);  // row sums R = K V
+    float err = ms > 0.f ? fabsf(U * X - ms) : 0.f, lsum;
     {
         // L_i = sum_j K_ij V_j C_ij with the cells reloaded (K is 0 off the
         // problem, where the loaded cost is 0 or a finite neighbour).
-        float l[H], ls[S];
+        float l[H];
 #pragma unroll
         for (int i = 0; i < H; ++i) {
             const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, r0 + i);
@@ -387,12 +328,12 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
             for (int t = 0; t < NC; ++t) acc = __builtin_fmaf(K[i][t] * wc[t], load_cell(rs, voff + 32 * t), acc);
             l[i] = acc;
         }
-        scatter<H>(l, ls, q);
-        lsum = ms > 0.f ? U * ls[0] : 0.f;
+        const float ls = row_totals<H>(l, tb, p, q);
+        lsum = ms > 0.f ? U * ls : 0.f;
     }
     gather_lds(xs[0]);
-    kmul<H, NC>(K, wc, X, q);  // column sums S = K^T U
-    err += ns > 0.f ? fabsf(V * X[0] - ns) : 0.f;
+    X = kmul<H, NC>(K, wc, tb, p, q);  // column sums S = K^T U
+    err += ns > 0.f ? fabsf(V * X - ns) : 0.f;
     err = wave_sum(err);
     lsum = wave_sum(lsum);
     if (lane == 0) {
