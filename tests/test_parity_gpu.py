@@ -269,7 +269,7 @@ def test_plain_early_stop_agrees_with_log(monkeypatch):
 
 # ---------------------------------------------------------------- symmetric shared cost, one wavefront per problem
 
-@pytest.mark.parametrize("d", [1, 2, 7, 8, 9, 16, 17, 33, 64, 65, 100, 104])
+@pytest.mark.parametrize("d", [1, 2, 7, 8, 9, 16, 17, 32, 33, 64, 65, 96, 97, 100, 104])
 def test_sym_kernel_shapes(d, monkeypatch):
     """Every register-tile width of the symmetric-cost kernel, ragged tails
     included; alone (plain) it solves every problem."""
