@@ -81,12 +81,28 @@ __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
     const float *al = A.alpha + (size_t)b * d1;
     const float *be = A.beta + (size_t)b * d2;
 
-    // Stage the cost (coalesced) and the potentials in LDS.
+    // Stage the cost (coalesced: thread t takes column t & 127 of every other
+    // row, d2 <= 128) and the potentials in LDS.
     if (t < d1) av[t] = al[t] * kLog2e;
     if (t < d2) bw[t] = be[t] * kLog2e;
-    for (int u = t; u < d1 * d2; u += kShThreads) {
-        const int i = u / d2, j = u - i * d2;
-        P[i * ld + j] = Cb[u];
+    // Eight loads in flight per thread before their stores: a load-store
+    // pair per row would wait out the memory latency once per row.
+    const int sj = t & (kShHalf - 1), si = t / kShHalf;
+    constexpr int kRs = kShThreads / kShHalf;  // rows per pass
+    if (sj < d2) {
+        for (int i0 = si; i0 < d1; i0 += 8 * kRs) {
+            float v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int i = i0 + kRs * k;
+                v[k] = i < d1 ? Cb[(size_t)i * d2 + sj] : 0.f;
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int i = i0 + kRs * k;
+                if (i < d1) P[i * ld + sj] = v[k];
+            }
+        }
     }
     __syncthreads();
 
@@ -99,6 +115,7 @@ __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
     if (own) {
         if (isrow) {
             const float a = av[k];
+#pragma unroll 4
             for (int j = 0; j < d2; ++j) {
                 const float c = P[k * ld + j];
                 const float p = ex2((a + bw[j]) - A.s * c);
@@ -107,6 +124,7 @@ __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
             }
         } else {
             const float bb = bw[k];
+#pragma unroll 4
             for (int i = 0; i < d1; ++i) {
                 const float c = P[i * ld + k];
                 const float p = ex2((av[i] + bb) - A.s * c);
@@ -116,9 +134,10 @@ __global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
         }
     }
     __syncthreads();  // the cost has been read: the plan overwrites it
-    for (int u = t; u < d1 * d2; u += kShThreads) {
-        const int i = u / d2, j = u - i * d2;
-        P[i * ld + j] = ex2((av[i] + bw[j]) - A.s * P[i * ld + j]);
+    if (sj < d2) {
+        const float bj = bw[sj];
+#pragma unroll 4
+        for (int i = si; i < d1; i += kRs) P[i * ld + sj] = ex2((av[i] + bj) - A.s * P[i * ld + sj]);
     }
     __syncthreads();
     const float mass = own ? (isrow ? A.mu[(size_t)b * d1 + k] : A.nu[(size_t)b * d2 + k]) : 0.f;
