@@ -16,203 +16,251 @@
 // the support).  Solved per problem by conjugate gradients preconditioned
 // with diag(H) = (r, c).
 //
-// One work-group of 256 threads per problem, max(d1, d2) <= 128: P lives in
-// LDS with an odd row stride (conflict-free both along rows and along
-// columns); thread t < 128 owns row t, thread 128 + t owns column t, so one
-// pass over P forms both halves of H p.  Reductions are fixed-order block
-// sums (deterministic).
+// One work-group of two wavefronts per problem, max(d1, d2) <= 8 N <= 128;
+// the plan lives in VGPRs.  Lane l = p + 8q (p = l & 7, q = l >> 3) of
+// wavefront w holds P[p + 8r][q + 8t] for its row blocks r in [w H, w H + H)
+// (H = ceil(N / 2)) and every column block t < N.  One pass over the
+// registers forms both halves of H p:
+//   rows:    partial sums over the lane's columns, summed over the 8 lanes q
+//            through a per-wavefront LDS transpose (lane (p, q < H) gets row
+//            p + 8 (w H + q));
+//   columns: partial sums over the lane's rows, summed over the 8 lanes p and
+//            the two wavefronts through LDS (thread c gets column c).
+// So a row i lives on one lane and a column j on thread j: every vector of
+// the conjugate-gradient iteration is kept there, and published to LDS for
+// the next product.  Reductions are fixed-order block sums (deterministic).
 #include "sk_device.h"
 #include "sk_internal.h"
 
 namespace sk {
 namespace {
 
-constexpr int kShThreads = 256;
-constexpr int kShHalf = kShThreads / 2;  // rows on threads [0, 128), columns on [128, 256)
-static_assert(kShHalf >= kSharpMaxD, "one thread per row and per column");
+constexpr int kShWaves = 2;
+constexpr int kVS = 20;  // LDS line stride of the published vectors (16-byte reads, 8 lines on distinct banks)
 
-__device__ __forceinline__ float block_sum(float v, float *red) {
-    v = wave_sum(v);
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    __syncthreads();
-    if (lane == 0) red[w] = v;
-    __syncthreads();
-    float s = 0.f;
+// Row totals through LDS: lane (p, q) holds partial sums x[r] of its rows
+// p + 8 (w H + r) over its column blocks; lane (p, r), r < NR, gets the total
+// of row r, summed over q in a fixed order.  tb: the wavefront's scratch of
+// 8 x 72 floats, entry (p, r, q) at p * 72 + r * 8 + q (the 64 writes of one
+// r on 64 distinct banks; each total two 16-byte reads).  A wavefront's LDS
+// operations complete in order: no barrier.
+template <int NR>
+__device__ __forceinline__ float row_totals(const float (&x)[NR], float *tb, int p, int q) {
+    static_assert(NR <= 8, "one row per lane q");
+    float *mine = tb + p * 72 + q;
 #pragma unroll
-    for (int k = 0; k < kShThreads / 64; ++k) s += red[k];
-    return s;
+    for (int r = 0; r < NR; ++r) mine[r * 8] = x[r];
+    __builtin_amdgcn_wave_barrier();
+    const float *row = tb + p * 72 + (q < NR ? q : NR - 1) * 8;
+    const float4 a = *reinterpret_cast<const float4 *>(row);
+    const float4 b = *reinterpret_cast<const float4 *>(row + 4);
+    __builtin_amdgcn_wave_barrier();
+    return ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w));
 }
 
-__host__ __device__ __forceinline__ int ld_of(int d2) { return d2 | 1; }  // odd row stride
-
-// sum_m a[m * stride] * v[m], m < n, from LDS: eight loads in flight and four
-// independent accumulators (a single chain would wait on every load).
-__device__ __forceinline__ float dot_lds(const float *a, int stride, const float *v, int n) {
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-    int m = 0;
-    for (; m + 8 <= n; m += 8) {
-        float x[8], y[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            x[u] = a[(m + u) * stride];
-            y[u] = v[m + u];
-        }
-        s0 = __builtin_fmaf(x[0], y[0], s0);
-        s1 = __builtin_fmaf(x[1], y[1], s1);
-        s2 = __builtin_fmaf(x[2], y[2], s2);
-        s3 = __builtin_fmaf(x[3], y[3], s3);
-        s0 = __builtin_fmaf(x[4], y[4], s0);
-        s1 = __builtin_fmaf(x[5], y[5], s1);
-        s2 = __builtin_fmaf(x[6], y[6], s2);
-        s3 = __builtin_fmaf(x[7], y[7], s3);
-    }
-    for (; m < n; ++m) s0 = __builtin_fmaf(a[m * stride], v[m], s0);
-    return (s0 + s1) + (s2 + s3);
+// Column partials: lane (p, q) of wavefront w writes its partial sum of
+// column q + 8t to cp[w][q + 8t][p] (64 consecutive floats per t); after a
+// barrier, column_total(c) sums column c's 16 partials in a fixed order.
+__device__ __forceinline__ int partial_at(int w, int p, int q, int t) { return (w * 128 + q + 8 * t) * 8 + p; }
+__device__ __forceinline__ float column_total(const float *cp, int c) {
+    const float4 *v0 = reinterpret_cast<const float4 *>(cp + c * 8);
+    const float4 *v1 = reinterpret_cast<const float4 *>(cp + (128 + c) * 8);
+    const float4 a = v0[0], b = v0[1], e = v1[0], f = v1[1];
+    return (((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w))) +
+           (((e.x + e.y) + (e.z + e.w)) + ((f.x + f.y) + (f.z + f.w)));
 }
 
-__global__ __launch_bounds__(kShThreads) void sk_sharp_kernel(SharpArgs A) {
-    extern __shared__ float P[];  // [d1][ld]: the cost first, then the plan
-    __shared__ float pv[2 * kShHalf];
-    __shared__ float av[kShHalf], bw[kShHalf];  // base-2 potentials
-    __shared__ float red[kShThreads / 64];
-    const int b = blockIdx.x, t = threadIdx.x;
-    const int d1 = A.d1, d2 = A.d2, ld = ld_of(d2);
+template <int N>
+__global__ __launch_bounds__(64 * kShWaves) __attribute__((amdgpu_waves_per_eu(2))) void sk_sharp_kernel(SharpArgs A) {
+    constexpr int H = (N + 1) / 2;
+    static_assert(8 * N <= 128 && H <= 8, "one thread per column, one lane per row");
+    // Published vectors: column j at colv[(j & 7) * kVS + (j >> 3)] (lane
+    // (p, q) reads line q), row p + 8 (w H + r) at rowv[p * kVS + 8 w + r]
+    // (lane (p, q) of wavefront w reads line p from entry 8w).
+    __shared__ __attribute__((aligned(16))) float colv[8 * kVS];
+    __shared__ __attribute__((aligned(16))) float rowv[8 * kVS];
+    __shared__ __attribute__((aligned(16))) float cp[2][kShWaves * 128 * 8];
+    __shared__ __attribute__((aligned(16))) float tsum[kShWaves][8 * 72];
+    __shared__ float bs[2][kShWaves][4];  // block-sum slots, alternating
+
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int p = lane & 7, q = lane >> 3;
+    const int b = blockIdx.x;
+    const int d1 = A.d1, d2 = A.d2;
+    const float s = A.s;
     const float *Cb = A.C + (A.c_batched ? (size_t)b * d1 * d2 : 0);
-    const float *al = A.alpha + (size_t)b * d1;
-    const float *be = A.beta + (size_t)b * d2;
+    float *const tb = tsum[w];
+    // Fixed-order sum over the work-group of n <= 4 values per thread; one
+    // barrier (a wavefront can be at most one sum ahead of the other, so two
+    // alternating slots suffice).
+    int slot = 0;
+    auto block_sum = [&](float(&v)[4], int n) {
+        for (int k = 0; k < n; ++k) v[k] = wave_sum(v[k]);
+        if (lane == 0)
+            for (int k = 0; k < n; ++k) bs[slot][w][k] = v[k];
+        __syncthreads();
+        for (int k = 0; k < n; ++k) v[k] = bs[slot][0][k] + bs[slot][1][k];
+        slot ^= 1;
+    };
 
-    // Stage the cost (coalesced: thread t takes column t & 127 of every other
-    // row, d2 <= 128) and the potentials in LDS.
-    if (t < d1) av[t] = al[t] * kLog2e;
-    if (t < d2) bw[t] = be[t] * kLog2e;
-    // Eight loads in flight per thread before their stores: a load-store
-    // pair per row would wait out the memory latency once per row.
-    const int sj = t & (kShHalf - 1), si = t / kShHalf;
-    constexpr int kRs = kShThreads / kShHalf;  // rows per pass
-    if (sj < d2) {
-        for (int i0 = si; i0 < d1; i0 += 8 * kRs) {
-            float v[8];
+    // The lane's cells: rows i = p + 8 (w H + ii), columns j = q + 8t.
+    float a2[H];  // base-2 potentials of the lane's rows
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int i = i0 + kRs * k;
-                v[k] = i < d1 ? Cb[(size_t)i * d2 + sj] : 0.f;
-            }
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int i = i0 + kRs * k;
-                if (i < d1) P[i * ld + sj] = v[k];
-            }
-        }
+    for (int ii = 0; ii < H; ++ii) {
+        const int i = p + 8 * (w * H + ii);
+        a2[ii] = i < d1 ? A.alpha[(size_t)b * d1 + i] * kLog2e : 0.f;
     }
-    __syncthreads();
+    // The plan P_ij = 2^(a_i + b_j - s C_ij) (0 off the problem), column
+    // block by column block, with the row partials of P and of P o C in
+    // registers and the column partials written out as each block is done.
+    float P[H][N];
+    float rP[H], rPC[H];
+#pragma unroll
+    for (int ii = 0; ii < H; ++ii) rP[ii] = rPC[ii] = 0.f;
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+        const int j = q + 8 * t;
+        const float bj = j < d2 ? A.beta[(size_t)b * d2 + j] * kLog2e : 0.f;
+        float cs = 0.f, csc = 0.f;
+#pragma unroll
+        for (int ii = 0; ii < H; ++ii) {
+            const int i = p + 8 * (w * H + ii);
+            const bool in = i < d1 && j < d2;
+            const float cij = in ? Cb[(size_t)i * d2 + j] : 0.f;
+            const float v = in ? ex2((a2[ii] + bj) - s * cij) : 0.f;
+            P[ii][t] = v;
+            rP[ii] += v;
+            rPC[ii] = __builtin_fmaf(v, cij, rPC[ii]);
+            cs += v;
+            csc = __builtin_fmaf(v, cij, csc);
+        }
+        cp[0][partial_at(w, p, q, t)] = cs;
+        cp[1][partial_at(w, p, q, t)] = csc;
+    }
 
-    const bool isrow = t < kShHalf;
-    const int k = isrow ? t : t - kShHalf;
-    const bool own = isrow ? k < d1 : k < d2;
-    // Diagonal of H (the plan's marginal) and the right-hand side (a or b),
-    // with the plan entries P_ij = 2^(a_i + b_j - s C_ij) formed on the way.
-    float dg = 0.f, rhs = 0.f;
-    if (own) {
-        if (isrow) {
-            const float a = av[k];
-#pragma unroll 4
-            for (int j = 0; j < d2; ++j) {
-                const float c = P[k * ld + j];
-                const float p = ex2((a + bw[j]) - A.s * c);
-                dg += p;
-                rhs = __builtin_fmaf(p, c, rhs);
-            }
-        } else {
-            const float bb = bw[k];
-#pragma unroll 4
-            for (int i = 0; i < d1; ++i) {
-                const float c = P[i * ld + k];
-                const float p = ex2((av[i] + bb) - A.s * c);
-                dg += p;
-                rhs = __builtin_fmaf(p, c, rhs);
-            }
-        }
-    }
-    __syncthreads();  // the cost has been read: the plan overwrites it
-    if (sj < d2) {
-        const float bj = bw[sj];
-#pragma unroll 4
-        for (int i = si; i < d1; i += kRs) P[i * ld + sj] = ex2((av[i] + bj) - A.s * P[i * ld + sj]);
-    }
+    // Owners: lane (p, q < H) owns row i = p + 8 (w H + q); thread c owns column c.
+    const int c = threadIdx.x;
+    const int i_own = p + 8 * (w * H + q);
+    const bool row_on = q < H && i_own < d1;
+    const bool col_on = c < d2;
+    // Diagonal of H (the plan's marginals) and the right-hand side (a, b).
+    float dgf = row_totals<H>(rP, tb, p, q);
+    float rf = row_totals<H>(rPC, tb, p, q);
     __syncthreads();
-    const float mass = own ? (isrow ? A.mu[(size_t)b * d1 + k] : A.nu[(size_t)b * d2 + k]) : 0.f;
-    const bool sup = own && mass > 0.f && dg > 0.f;
-    if (!sup) {
-        dg = 0.f;
-        rhs = 0.f;
-    }
+    float dgg = col_on ? column_total(cp[0], c) : 0.f;
+    float rg = col_on ? column_total(cp[1], c) : 0.f;
+    const float mf = row_on ? A.mu[(size_t)b * d1 + i_own] : 0.f;
+    const float mg = col_on ? A.nu[(size_t)b * d2 + c] : 0.f;
+    const bool supf = row_on && mf > 0.f && dgf > 0.f;
+    const bool supg = col_on && mg > 0.f && dgg > 0.f;
+    if (!supf) dgf = rf = 0.f;
+    if (!supg) dgg = rg = 0.f;
     // Project the right-hand side off (1, -1) over the supports.
     {
-        const float sgn = isrow ? 1.f : -1.f;
-        const float dot = block_sum(sup ? sgn * rhs : 0.f, red);
-        const float n = block_sum(sup ? 1.f : 0.f, red);
-        if (sup) rhs -= sgn * (dot / n);
+        float v[4] = {(supf ? rf : 0.f) - (supg ? rg : 0.f), (supf ? 1.f : 0.f) + (supg ? 1.f : 0.f), 0.f, 0.f};
+        block_sum(v, 2);
+        if (supf) rf -= v[0] / v[1];
+        if (supg) rg += v[0] / v[1];
     }
 
-    // Jacobi-preconditioned conjugate gradients; every scalar below is a
-    // block sum, so the control flow is uniform across the work-group.
-    float x = 0.f, r = rhs;
-    float z = sup ? r / dg : 0.f, p = z;
-    float rz = block_sum(r * z, red);
+    // Jacobi-preconditioned conjugate gradients; every scalar is a block sum,
+    // so the control flow is uniform across the work-group.
+    float xf = 0.f, xg = 0.f;
+    float zf = supf ? rf / dgf : 0.f, zg = supg ? rg / dgg : 0.f;
+    float pf = zf, pg = zg;
+    float rz;
+    {
+        float v[4] = {rf * zf + rg * zg, 0.f, 0.f, 0.f};
+        block_sum(v, 1);
+        rz = v[0];
+    }
     const float stop = A.cg_tol * A.cg_tol * rz;
     int it = 0;
     if (rz > 0.f) {
         while (it < A.max_cg) {
-            if (own) pv[isrow ? k : kShHalf + k] = p;
+            // Publish p; its row half and its column half meet the plan.
+            if (q < H) rowv[p * kVS + 8 * w + q] = pf;
+            if (c < 8 * N) colv[(c & 7) * kVS + (c >> 3)] = pg;
             __syncthreads();
-            float q = dg * p;
-            if (sup) q += isrow ? dot_lds(P + k * ld, 1, pv + kShHalf, d2) : dot_lds(P + k, ld, pv, d1);
-            const float pq = block_sum(p * q, red);  // its barriers also retire the reads of pv
+            float wc[N], wr[H];
+#pragma unroll
+            for (int t = 0; t < N; ++t) wc[t] = colv[q * kVS + t];
+#pragma unroll
+            for (int ii = 0; ii < H; ++ii) wr[ii] = rowv[p * kVS + 8 * w + ii];
+            // One pass over the plan: row partials against the column half
+            // of p, column partials against the row half (written out per
+            // column block).
+            float yr[H];
+#pragma unroll
+            for (int ii = 0; ii < H; ++ii) yr[ii] = 0.f;
+#pragma unroll
+            for (int t = 0; t < N; ++t) {
+                float yc = 0.f;
+#pragma unroll
+                for (int ii = 0; ii < H; ++ii) {
+                    yr[ii] = __builtin_fmaf(P[ii][t], wc[t], yr[ii]);
+                    yc = __builtin_fmaf(P[ii][t], wr[ii], yc);
+                }
+                cp[0][partial_at(w, p, q, t)] = yc;
+            }
+            const float Pp = row_totals<H>(yr, tb, p, q);  // (P p_g)_i on the row owner
+            __syncthreads();
+            const float PTp = col_on ? column_total(cp[0], c) : 0.f;  // (P^T p_f)_j on the column owner
+            const float qf = supf ? __builtin_fmaf(dgf, pf, Pp) : 0.f;
+            const float qg = supg ? __builtin_fmaf(dgg, pg, PTp) : 0.f;
+            float v[4] = {pf * qf + pg * qg, 0.f, 0.f, 0.f};
+            block_sum(v, 1);  // its barrier also retires this product's reads of cp, colv and rowv
+            const float pq = v[0];
             if (!(pq > 0.f)) break;
             const float step = rz / pq;
-            x = __builtin_fmaf(step, p, x);
-            r = __builtin_fmaf(-step, q, r);
-            z = sup ? r / dg : 0.f;
-            const float rzn = block_sum(r * z, red);
+            xf = __builtin_fmaf(step, pf, xf);
+            xg = __builtin_fmaf(step, pg, xg);
+            rf = __builtin_fmaf(-step, qf, rf);
+            rg = __builtin_fmaf(-step, qg, rg);
+            zf = supf ? rf / dgf : 0.f;
+            zg = supg ? rg / dgg : 0.f;
+            float u[4] = {rf * zf + rg * zg, 0.f, 0.f, 0.f};
+            block_sum(u, 1);
+            const float rzn = u[0];
             ++it;
             if (!(rzn > stop)) break;
-            p = __builtin_fmaf(rzn / rz, p, z);
+            pf = __builtin_fmaf(rzn / rz, pf, zf);
+            pg = __builtin_fmaf(rzn / rz, pg, zg);
             rz = rzn;
         }
     }
 
     // Centre each block over its support, scale by the upstream gradient.
-    const float sx_r = block_sum(sup && isrow ? x : 0.f, red);
-    const float n_r = block_sum(sup && isrow ? 1.f : 0.f, red);
-    const float sx_c = block_sum(sup && !isrow ? x : 0.f, red);
-    const float n_c = block_sum(sup && !isrow ? 1.f : 0.f, red);
+    float v[4] = {supf ? xf : 0.f, supf ? 1.f : 0.f, supg ? xg : 0.f, supg ? 1.f : 0.f};
+    block_sum(v, 4);
     const float g = A.grad_loss[b];
-    if (own) {
-        const float mean = isrow ? (n_r > 0.f ? sx_r / n_r : 0.f) : (n_c > 0.f ? sx_c / n_c : 0.f);
-        const float v = sup ? g * (x - mean) : 0.f;
-        if (isrow)
-            A.grad_mu[(size_t)b * d1 + k] = v;
-        else
-            A.grad_nu[(size_t)b * d2 + k] = v;
+    if (row_on) {
+        const float mean = v[1] > 0.f ? v[0] / v[1] : 0.f;
+        A.grad_mu[(size_t)b * d1 + i_own] = supf ? g * (xf - mean) : 0.f;
     }
-    if (t == 0 && A.cg_iters) A.cg_iters[b] = it;
+    if (col_on) {
+        const float mean = v[3] > 0.f ? v[2] / v[3] : 0.f;
+        A.grad_nu[(size_t)b * d2 + c] = supg ? g * (xg - mean) : 0.f;
+    }
+    if (threadIdx.x == 0 && A.cg_iters) A.cg_iters[b] = it;
 }
 
-size_t sharp_lds_bytes(int d1, int d2) { return sizeof(float) * (size_t)d1 * ld_of(d2); }
+template <int N>
+hipError_t launch_n(const SharpArgs &a, hipStream_t st) {
+    hipLaunchKernelGGL((sk_sharp_kernel<N>), dim3(a.B), dim3(64 * kShWaves), 0, st, a);
+    return hipGetLastError();
+}
 
 }  // namespace
 
 hipError_t launch_sharp(const SharpArgs &a, hipStream_t st) {
-    const size_t lds = sharp_lds_bytes(a.d1, a.d2);
-    static bool attr = false;  // above 64 KB of LDS (d near 128) needs the larger dynamic limit
-    if (!attr) {
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_sharp_kernel),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)sharp_lds_bytes(kSharpMaxD, kSharpMaxD));
-        attr = true;
-    }
-    hipLaunchKernelGGL(sk_sharp_kernel, dim3(a.B), dim3(kShThreads), lds, st, a);
-    return hipGetLastError();
+    const int nb = ((a.d1 > a.d2 ? a.d1 : a.d2) + 7) / 8;  // at most kSharpMaxD / 8 = 16
+    if (nb <= 2) return launch_n<2>(a, st);
+    if (nb <= 4) return launch_n<4>(a, st);
+    if (nb <= 8) return launch_n<8>(a, st);
+    if (nb <= 13) return launch_n<13>(a, st);
+    return launch_n<16>(a, st);
 }
 
 }  // namespace sk

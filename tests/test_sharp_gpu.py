@@ -61,7 +61,8 @@ def test_sharp_label_full_batch_sampled():
     check_sharp(workloads.make_config(2), idx=np.array([0, 1, 255, 511, 512, 700, 1022, 1023]))
 
 
-@pytest.mark.parametrize("d1,d2", [(1, 7), (7, 1), (17, 9), (37, 100), (64, 64), (100, 37), (128, 128), (127, 33)])
+@pytest.mark.parametrize("d1,d2", [(1, 7), (7, 1), (16, 16), (17, 9), (32, 5), (37, 100), (64, 64), (100, 37),
+                                   (104, 104), (105, 10), (128, 128), (127, 33)])
 def test_sharp_shapes(d1, d2):
     prob = workloads.random_problem(seed=400 + d1 + d2, B=4, d1=d1, d2=d2, lam=0.1, n_iter=200)
     check_sharp(prob)
