@@ -30,18 +30,17 @@ PEAK_HBM_GBS = 8000.0
 # v_exp_f32 issues a wave64 in 8 cycles per SIMD (half rate; measured 28.9 of
 # 32 per clock per CU in a pure-exp loop): 256 CUs x 4 SIMDs x 8 lanes/clk x 2.4 GHz
 PEAK_EXP_TS = 256 * 4 * 8 * 2.4e9 / 1e12
-# MI355X published dense fp32 peaks (TFLOP/s): matrix cores, and vector ALU.
-PEAK_FP32_MFMA = 157.3
+# MI355X published dense fp32 vector peak (TFLOP/s).
 PEAK_FP32_VALU = 157.3
 
 # Resident kernels: the first choice for a shape and the source it is built
-# from.  A shared symmetric cost with d1 = d2 <= 104: one work-group per problem
-# on the vector ALU; another shared cost: matrix cores; a per-sample cost: the
-# plain form on the vector ALU.
+# from, both the plain form on the vector ALU with K in registers.  A shared
+# symmetric cost with d1 = d2 <= 104: the symmetric kernel; any other cost
+# (shared or per sample): the general kernel.
 RESIDENT_KERNELS = {
     "sym": ("sk_resident_sym_kernel", "sk_resident_sym.hip", "alu", PEAK_FP32_VALU),
-    "shared": ("sk_resident_mfma_kernel", "sk_resident_mfma.hip", "mfma", PEAK_FP32_MFMA),
-    "batched": ("sk_resident_plain_kernel", "sk_resident_plain.hip", "alu", PEAK_FP32_VALU),
+    "shared": ("sk_resident_gen_kernel", "sk_resident_gen.hip", "alu", PEAK_FP32_VALU),
+    "batched": ("sk_resident_gen_kernel", "sk_resident_gen.hip", "alu", PEAK_FP32_VALU),
 }
 
 

@@ -61,10 +61,10 @@ sk::BwdArgs bwd_args(const sk_problem *p, const float *grad_loss, const float *m
 }
 
 // Resident regime.  First choice: the symmetric-cost kernel (shared cost,
-// d1 = d2 <= 104), else the matrix-core kernel (shared cost), else the
-// per-sample plain-form kernel.  Each hands over what it cannot solve: the
-// symmetric kernel to the matrix-core kernel (iters = -2), every plain form
-// to the log-domain kernel (iters = -1).  Launches on one stream, in order.
+// d1 = d2 <= 104), else the general plain-form kernel (any cost).  Each
+// hands over what it cannot solve: the symmetric kernel to the general
+// kernel (iters = -2), both plain forms to the log-domain kernel
+// (iters = -1).  Launches on one stream, in order.
 hipError_t launch_resident_regime(sk::FwdArgs a, int form, hipStream_t s) {
     if (form == kFormLog) return sk::launch_resident(a, s);
     hipError_t e = hipSuccess;
@@ -73,10 +73,10 @@ hipError_t launch_resident_regime(sk::FwdArgs a, int form, hipStream_t s) {
         ran = true;
         if (e == hipSuccess && form != kFormPlain) {
             a.only_flagged = 2;
-            if (!sk::launch_resident_mfma(a, s, &e)) return hipErrorInvalidValue;  // takes every shape the first takes
+            if (!sk::launch_resident_gen(a, s, &e)) return hipErrorInvalidValue;  // takes every shape the first takes
         }
     } else {
-        ran = sk::launch_resident_mfma(a, s, &e) || sk::launch_resident_plain(a, s, &e);
+        ran = sk::launch_resident_gen(a, s, &e);
     }
     if (!ran) return sk::launch_resident(a, s);
     if (e != hipSuccess || form == kFormPlain) return e;

@@ -98,4 +98,46 @@ __device__ __forceinline__ float tree_sum(const float *v) {
     }
 }
 
+// ---- register-resident products: lane (p, q) of a wavefront, p = lane & 7,
+// q = lane >> 3, holds cells [p + 8r][q + 8t] of an 8-row by 8-column block
+// grid ----
+
+// Row totals through LDS: lane (p, q) holds partial sums x[r] of its rows
+// p + 8r (r < NR) over its column blocks; lane (p, r), r < NR, gets the total
+// of row r, summed over q in a fixed order (other lanes a copy of row
+// NR - 1).  tb: the wavefront's own scratch of 8 x 72 floats, entry (p, r, q)
+// at p * 72 + r * 8 + q, so that the 64 writes of one r fall on 64 distinct
+// banks and each total is two 16-byte reads.  The LDS operations of one
+// wavefront complete in order, so no barrier is needed, and the next call's
+// writes cannot overtake this call's reads.
+constexpr int kRowTotalsFloats = 8 * 72;
+template <int NR>
+__device__ __forceinline__ float row_totals(const float (&x)[NR], float *tb, int p, int q) {
+    static_assert(NR <= 8, "one row per lane q");
+    float *mine = tb + p * 72 + q;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) mine[r * 8] = x[r];
+    __builtin_amdgcn_wave_barrier();
+    const float *row = tb + p * 72 + (q < NR ? q : NR - 1) * 8;
+    const float4 a = *reinterpret_cast<const float4 *>(row);
+    const float4 b = *reinterpret_cast<const float4 *>(row + 4);
+    __builtin_amdgcn_wave_barrier();
+    return ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w));
+}
+
+// Column partials of a two-wavefront work-group: lane (p, q) of wavefront w
+// writes its partial sum of column q + 8t to cp[partial_at(w, p, q, t)]
+// (64 consecutive floats per t); after a barrier column_total(cp, c) sums
+// column c's 16 partials (8 lanes p, 2 wavefronts) in a fixed order.
+// cp holds kColumnPartialsFloats floats (columns < 128), 16-byte aligned.
+constexpr int kColumnPartialsFloats = 2 * 128 * 8;
+__device__ __forceinline__ int partial_at(int w, int p, int q, int t) { return (w * 128 + q + 8 * t) * 8 + p; }
+__device__ __forceinline__ float column_total(const float *cp, int c) {
+    const float4 *v0 = reinterpret_cast<const float4 *>(cp + c * 8);
+    const float4 *v1 = reinterpret_cast<const float4 *>(cp + (128 + c) * 8);
+    const float4 a = v0[0], b = v0[1], e = v1[0], f = v1[1];
+    return (((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w))) +
+           (((e.x + e.y) + (e.z + e.w)) + ((f.x + f.y) + (f.z + f.w)));
+}
+
 }  // namespace sk

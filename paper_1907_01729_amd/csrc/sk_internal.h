@@ -37,17 +37,17 @@ constexpr int kResidentMaxD = 128;
 
 bool resident_fits(int d1, int d2);
 hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
-// Plain-form resident kernel: returns false (and launches nothing) when it
-// does not take the shape; otherwise *err is the launch status.  Problems it
-// cannot keep in range come back with iters = -1.
-bool launch_resident_plain(const FwdArgs &a, hipStream_t st, hipError_t *err);
-// Same contract; a cost shared by the batch only, products on the matrix cores.
-// With only_flagged = 2 it solves the problems marked iters = -2.
-bool launch_resident_mfma(const FwdArgs &a, hipStream_t st, hipError_t *err);
-// Same contract; a shared cost with d1 = d2 <= 104, one wavefront per problem
+// Plain-form resident kernels: each returns false (and launches nothing) when
+// it does not take the shape; otherwise *err is the launch status.  Problems
+// it cannot keep in range come back with iters = -1.
+// A shared cost with d1 = d2 <= 104, two wavefronts per problem
 // on the vector ALU.  A cost that is not symmetric marks every problem with
-// iters = -2 (for the matrix-core kernel).
+// iters = -2 (for the general kernel).
 bool launch_resident_sym(const FwdArgs &a, hipStream_t st, hipError_t *err);
+// Same contract; any cost (shared or per problem) with max(d1, d2) <= 128,
+// two wavefronts per problem on the vector ALU.  With only_flagged = 2 it
+// solves the problems marked iters = -2.
+bool launch_resident_gen(const FwdArgs &a, hipStream_t st, hipError_t *err);
 
 // The tiled sweep keeps a whole cost row in one wavefront's registers.
 constexpr int kTiledMaxD2 = 4096;

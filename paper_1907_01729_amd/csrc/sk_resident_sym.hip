@@ -6,7 +6,7 @@
 // With K = 2^(cl - clmax) (cl = -C log2(e)/lambda, clmax = max cl) the
 // iteration is R = K V, U = mu / R, S = K^T U, V = nu / S, from u^0 = 1 on
 // the support of mu: the same iterates, range guards and outputs as the
-// matrix-core kernel (alpha = ln2 log2 U, beta = ln2 (log2 V - clmax)), so the
+// general kernel (alpha = ln2 log2 U, beta = ln2 (log2 V - clmax)), so the
 // potentials equal the log-domain iterates up to rounding.
 //
 // Lane l = p + 8q (p = l & 7, q = l >> 3) of wavefront w holds K[p + 8r][q + 8t]
@@ -23,7 +23,7 @@
 //
 // The kernel verifies the symmetry of the cost first, pair by pair (bit
 // equality); a cost that is not symmetric marks every problem with iters = -2
-// for the matrix-core kernel, launched next.  A problem outside the plain
+// for the general kernel, launched next.  A problem outside the plain
 // form's range gets iters = -1 (the log-domain kernel takes it): a cost
 // spread wider than the range at the start, or a guard that failed in any
 // iteration (checked once, at the end): a sum R_i, S_j outside
@@ -42,28 +42,6 @@ constexpr float kRangeBits = 64.f;
 
 __device__ __forceinline__ bool sum_ok(float x) { return x >= kLo && x <= kHi; }
 __device__ __forceinline__ bool scale_ok(float x) { return x >= kSMin && x <= kSMax; }
-
-// Row totals through LDS: lane (p, q) holds partial sums x[r] of rows
-// p + 8 (r0 + r) over its column blocks; lane (p, r), r < NR, gets the total
-// of its row r, summed over q in a fixed order (other lanes get a copy of
-// row NR - 1).  tb is the wavefront's own scratch of 8 x 72 floats, entry
-// (p, r, q) at p * 72 + r * 8 + q: the 64 writes of one r fall on 64
-// distinct banks and each total is two 16-byte reads.  The LDS operations of
-// one wavefront complete in order, so no barrier is needed, and the next
-// call's writes cannot overtake this call's reads.
-template <int NR>
-__device__ __forceinline__ float row_totals(const float (&x)[NR], float *tb, int p, int q) {
-    static_assert(NR <= 8, "one row per lane q");
-    float *mine = tb + p * 72 + q;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) mine[r * 8] = x[r];
-    __builtin_amdgcn_wave_barrier();
-    const float *row = tb + p * 72 + (q < NR ? q : NR - 1) * 8;
-    const float4 a = *reinterpret_cast<const float4 *>(row);
-    const float4 b = *reinterpret_cast<const float4 *>(row + 4);
-    __builtin_amdgcn_wave_barrier();
-    return ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w));
-}
 
 // (K w) of the lane's row for the column-layout w (NR row blocks).
 template <int NR, int NC>
@@ -111,7 +89,7 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     // the next iteration's barriers.
     __shared__ __attribute__((aligned(16))) float red[2][2][2];
     __shared__ float ini[2][2][4];  // set-up exchanges
-    __shared__ __attribute__((aligned(16))) float tsum[2][8 * 72];  // per-wavefront row-total scratch
+    __shared__ __attribute__((aligned(16))) float tsum[2][kRowTotalsFloats];  // per-wavefront row-total scratch
 
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: descriptors stay scalar

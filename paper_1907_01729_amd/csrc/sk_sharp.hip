@@ -17,7 +17,7 @@
 // with diag(H) = (r, c).
 //
 // One work-group of two wavefronts per problem, max(d1, d2) <= 8 N <= 128;
-// the plan lives in VGPRs.  Lane l = p + 8q (p = l & 7, q = l >> 3) of
+// the plan lives in VGPRs (the products are those of sk_device.h).  Lane l = p + 8q (p = l & 7, q = l >> 3) of
 // wavefront w holds P[p + 8r][q + 8t] for its row blocks r in [w H, w H + H)
 // (H = ceil(N / 2)) and every column block t < N.  One pass over the
 // registers forms both halves of H p:
@@ -38,38 +38,6 @@ namespace {
 constexpr int kShWaves = 2;
 constexpr int kVS = 20;  // LDS line stride of the published vectors (16-byte reads, 8 lines on distinct banks)
 
-// Row totals through LDS: lane (p, q) holds partial sums x[r] of its rows
-// p + 8 (w H + r) over its column blocks; lane (p, r), r < NR, gets the total
-// of row r, summed over q in a fixed order.  tb: the wavefront's scratch of
-// 8 x 72 floats, entry (p, r, q) at p * 72 + r * 8 + q (the 64 writes of one
-// r on 64 distinct banks; each total two 16-byte reads).  A wavefront's LDS
-// operations complete in order: no barrier.
-template <int NR>
-__device__ __forceinline__ float row_totals(const float (&x)[NR], float *tb, int p, int q) {
-    static_assert(NR <= 8, "one row per lane q");
-    float *mine = tb + p * 72 + q;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) mine[r * 8] = x[r];
-    __builtin_amdgcn_wave_barrier();
-    const float *row = tb + p * 72 + (q < NR ? q : NR - 1) * 8;
-    const float4 a = *reinterpret_cast<const float4 *>(row);
-    const float4 b = *reinterpret_cast<const float4 *>(row + 4);
-    __builtin_amdgcn_wave_barrier();
-    return ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w));
-}
-
-// Column partials: lane (p, q) of wavefront w writes its partial sum of
-// column q + 8t to cp[w][q + 8t][p] (64 consecutive floats per t); after a
-// barrier, column_total(c) sums column c's 16 partials in a fixed order.
-__device__ __forceinline__ int partial_at(int w, int p, int q, int t) { return (w * 128 + q + 8 * t) * 8 + p; }
-__device__ __forceinline__ float column_total(const float *cp, int c) {
-    const float4 *v0 = reinterpret_cast<const float4 *>(cp + c * 8);
-    const float4 *v1 = reinterpret_cast<const float4 *>(cp + (128 + c) * 8);
-    const float4 a = v0[0], b = v0[1], e = v1[0], f = v1[1];
-    return (((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w))) +
-           (((e.x + e.y) + (e.z + e.w)) + ((f.x + f.y) + (f.z + f.w)));
-}
-
 template <int N>
 __global__ __launch_bounds__(64 * kShWaves) __attribute__((amdgpu_waves_per_eu(2))) void sk_sharp_kernel(SharpArgs A) {
     constexpr int H = (N + 1) / 2;
@@ -79,8 +47,8 @@ __global__ __launch_bounds__(64 * kShWaves) __attribute__((amdgpu_waves_per_eu(2
     // (lane (p, q) of wavefront w reads line p from entry 8w).
     __shared__ __attribute__((aligned(16))) float colv[8 * kVS];
     __shared__ __attribute__((aligned(16))) float rowv[8 * kVS];
-    __shared__ __attribute__((aligned(16))) float cp[2][kShWaves * 128 * 8];
-    __shared__ __attribute__((aligned(16))) float tsum[kShWaves][8 * 72];
+    __shared__ __attribute__((aligned(16))) float cp[2][kColumnPartialsFloats];
+    __shared__ __attribute__((aligned(16))) float tsum[kShWaves][kRowTotalsFloats];
     __shared__ float bs[2][kShWaves][4];  // block-sum slots, alternating
 
     const int lane = threadIdx.x & 63;

@@ -96,7 +96,7 @@ def check_backward(prob, gpu, ref, idx=None, grad_C=False, seed=0):
 def form(request, monkeypatch):
     """Resident regime: the plain-form kernels with their fallbacks (the
     default), the same without the symmetric-cost kernel (symmetric costs go
-    to the matrix-core kernel), or the log-domain kernel alone."""
+    to the general kernel), or the log-domain kernel alone."""
     monkeypatch.setenv("SK_RESIDENT_FORM", request.param)
     return request.param
 
@@ -287,7 +287,7 @@ def test_sym_kernel_zero_masses(monkeypatch):
 
 
 def test_sym_kernel_hands_over_asymmetric_cost(monkeypatch):
-    """An asymmetric cost (one pair differs) is handed to the matrix-core
+    """An asymmetric cost (one pair differs) is handed to the general
     kernel: iters = -2 from the symmetric kernel alone, and with the fallback
     the same bits as the path without the symmetric kernel."""
     prob = workloads.random_problem(seed=32, B=6, d1=50, d2=50, lam=0.1, n_iter=50, cost="sym")
@@ -331,6 +331,43 @@ def test_sym_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
     check_backward(prob, gpu, ref)
     for k in ("alpha", "beta", "loss", "marg_err", "iters"):
         np.testing.assert_array_equal(gpu[k][rest], alone[k][rest])
+
+
+@pytest.mark.parametrize("tol,n_iter", [(0.0, 50), (1e-5, 300)])
+def test_gen_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
+    """Per-sample costs, d1 != d2: a tiny positive mass (1e-37) fails a guard
+    of the general kernel inside the iteration; alone it returns that
+    problem unsolved and the rest solved, with the fallback the problem
+    matches the oracle and the others keep their bits."""
+    prob = workloads.random_problem(seed=38, B=5, d1=60, d2=45, lam=0.1, n_iter=n_iter, c_batched=True, tol=tol)
+    prob.mu[1, 9] = 1e-37
+    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    alone = _gpu(prob)
+    rest = np.arange(prob.B) != 1
+    assert alone["iters"][1] == -1
+    assert np.all(alone["iters"][rest] >= 1)
+    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+    for k in ("alpha", "beta", "loss", "marg_err", "iters"):
+        np.testing.assert_array_equal(gpu[k][rest], alone[k][rest])
+
+
+def test_gen_kernel_full_batch_per_sample_sampled():
+    """The general kernel at the label workload's launch size with one cost
+    per problem (B=1024, d=100); the oracle checks a sample."""
+    base = workloads.make_config(2)
+    rng = np.random.default_rng(39)
+    C = (base.C[0][None] * rng.uniform(0.75, 1.05, size=(base.B, 1, 1))).astype(np.float32)  # spread <= 57 bits
+    C[:, 3, 5] += 0.05  # not symmetric
+    prob = workloads.random_problem(seed=39, B=base.B, d1=100, d2=100, lam=base.lam, n_iter=base.n_iter,
+                                    c_batched=True)
+    prob.C = C
+    gpu = _gpu(prob)
+    assert np.all(gpu["iters"] == prob.n_iter)
+    idx = np.array([0, 1, 300, 511, 512, 901, 1023])
+    gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx, grad_C=True)
 
 
 def test_sym_kernel_early_stop(monkeypatch):
