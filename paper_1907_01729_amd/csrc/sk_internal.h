@@ -58,7 +58,8 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);
 hipError_t launch_backward(const BwdArgs &a, hipStream_t st);
 
 // Gradient of the sharp loss E^0 (implicit differentiation of the plan,
-// conjugate gradients per problem); the plan of one problem sits in LDS.
+// conjugate gradients per problem); the plan of one problem sits in the
+// VGPRs of its two wavefronts.
 constexpr int kSharpMaxD = 128;
 struct SharpArgs {
     const float *grad_loss, *mu, *nu, *C, *alpha, *beta;
