@@ -577,3 +577,31 @@ def test_shared_sweep_early_stop_compaction(monkeypatch):
     assert (its < prob.n_iter).sum() >= prob.B - 2 and len(set(its.tolist())) > 3, its
     for k in plain:
         np.testing.assert_array_equal(gpu[k], plain[k])
+
+
+# ---------------------------------------------------------------- randomized resident problems
+
+def test_random_resident_problems(monkeypatch):
+    """Forty seeded random problems of the resident regime (d1, d2 <= 128,
+    shared or per-sample, symmetric or not, zero masses, lambda over two
+    decades so that some leave the plain form's range, fixed or early-stopped
+    iterations), through whichever kernels take them, forward and backward
+    against the oracle."""
+    rng = np.random.default_rng(2024)
+    for case in range(40):
+        d1, d2 = int(rng.integers(1, 129)), int(rng.integers(1, 129))
+        if rng.random() < 0.3:
+            d2 = d1
+        B = int(rng.integers(1, 10))
+        lam = float(10 ** rng.uniform(-1.7, 0.3))
+        n_iter = int(rng.integers(0, 120))
+        tol = float(rng.choice([0.0, 0.0, 1e-4, 1e-5]))
+        cb = bool(rng.random() < 0.4)
+        zf = float(rng.choice([0.0, 0.0, 0.2]))
+        cost = "sym" if (d1 == d2 and rng.random() < 0.6) else "uniform"
+        monkeypatch.setenv("SK_RESIDENT_FORM", "nosym" if rng.random() < 0.25 else "auto")
+        prob = workloads.random_problem(seed=int(rng.integers(1 << 30)), B=B, d1=d1, d2=d2, lam=lam,
+                                        n_iter=n_iter, c_batched=cb, zero_frac=zf, cost=cost, tol=tol)
+        _say(f"[random {case}]")
+        gpu, ref = check_forward(prob)
+        check_backward(prob, gpu, ref, grad_C=True)

@@ -123,3 +123,20 @@ def test_sharp_autograd_wrapper():
     ref = oracle.sharp_gradient(np.arange(1, 5), prob.mu, prob.nu, prob.C, prob.lam, a, b)
     assert rel_err_rows(mu.grad.cpu().numpy(), ref["grad_mu"]) <= GRAD_RTOL
     assert rel_err_rows(nu.grad.cpu().numpy(), ref["grad_nu"]) <= GRAD_RTOL
+
+
+def test_sharp_random_problems():
+    """Twenty seeded random problems (d1, d2 <= 128, shared or per-sample,
+    symmetric or not, zero masses, lambda in [0.05, 1]) against the dense solve."""
+    rng = np.random.default_rng(77)
+    for case in range(20):
+        d1, d2 = int(rng.integers(1, 129)), int(rng.integers(1, 129))
+        if rng.random() < 0.3:
+            d2 = d1
+        cost = "sym" if (d1 == d2 and rng.random() < 0.5) else "uniform"
+        prob = workloads.random_problem(seed=int(rng.integers(1 << 30)), B=int(rng.integers(1, 7)), d1=d1, d2=d2,
+                                        lam=float(10 ** rng.uniform(-1.3, 0.0)), n_iter=int(rng.integers(100, 400)),
+                                        c_batched=bool(rng.random() < 0.4), zero_frac=float(rng.choice([0.0, 0.0, 0.2])),
+                                        cost=cost)
+        _say(f"[random {case}]")
+        check_sharp(prob, seed=case)
