@@ -56,9 +56,9 @@ __device__ __forceinline__ float kmul(const float (&K)[NR][NC], const float (&wc
     return row_totals<NR>(x, tb, p, q);
 }
 
-// Buffer descriptor over the cost from row 8r on (reads past the end of the
-// cost return 0); one per row block, so that a lane's byte offset into it is
-// the same register for every block and the column block an immediate.
+// Buffer descriptor over the d x d cost from row 8r on (reads past its end
+// return 0): a lane's column is the register offset, the row block an
+// immediate or a scalar offset.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t block_rsrc(const float *C, int d, int r) {
     const int rest = d * d - 8 * r * d;
     return __builtin_amdgcn_make_buffer_rsrc((void *)(C + (size_t)8 * r * d), (short)0, rest > 0 ? 4 * rest : 0,
@@ -99,28 +99,67 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     const float s = A.s;
     const int r0 = w * H;  // first row block of this wavefront
 
-    // Raw cost cells of the wavefront's row blocks, and the transposed cells
-    // (q + 8t, p + 8r) for the symmetry check: rows past d read 0, columns
-    // past d the next row's cells; every such cell is masked.
-    const int voff = (p * d + q) * 4, toff = (q * d + p) * 4;
+    // Raw cost cells of the wavefront's row blocks and the symmetry check, the
+    // cost streamed through LDS one row block (8 rows) at a time: thread tau
+    // stages column tau of the block (coalesced loads, 0 past d), the
+    // wavefront owning the block takes its cells from it, and every pair
+    // {(x, y), (y, x)} is compared when the later of its two row blocks is
+    // staged, by the owner of the earlier one (whose cells are all loaded by
+    // then).  Cells off the problem are masked (row block r holds a row iff
+    // r < rlim, column block t a column iff t < tlim).
     const int rlim = (d - p + 7) >> 3, tlim = (d - q + 7) >> 3;
+    constexpr int LDC = 136;             // = 8 mod 64: row reads (p, q + 8t) and transposed reads (q, p + 8a) hit 64 banks
+    constexpr int PF = NC < 4 ? NC : 4;  // row blocks in flight
+    __shared__ __attribute__((aligned(16))) float cst[2][8 * LDC];
+    const int tau = threadIdx.x;
+    const __amdgpu_buffer_rsrc_t whole = block_rsrc(A.C, d, 0);
+    // Stream row blocks 0 .. NC-1 through LDS (PF in flight, one barrier per
+    // block) and hand each staged block to visit(c, block).  Block c goes
+    // into buffer c & 1, whose previous block was read before the last
+    // barrier; rows and columns past d are staged as 0.
+    auto stream_blocks = [&](auto &&visit) {
+        float pf[PF][8];
+        auto load_block = [&](int c, float(&v)[8]) {
+#pragma unroll
+            for (int rr = 0; rr < 8; ++rr)
+                v[rr] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(whole, tau * 4, (8 * c + rr) * d * 4, 0));
+        };
+#pragma unroll
+        for (int c = 0; c < PF; ++c) load_block(c, pf[c]);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            if (tau < 8 * NC)
+#pragma unroll
+                for (int rr = 0; rr < 8; ++rr) cst[c & 1][rr * LDC + tau] = tau < d ? pf[c % PF][rr] : 0.f;
+            if (c + PF < NC) load_block(c + PF, pf[c % PF]);
+            __syncthreads();
+            visit(c, static_cast<const float *>(cst[c & 1]));
+        }
+    };
     float K[H][NC];
+    if (2 * H > NC && w == 1)  // the padding row block past 8 NC rows is never staged
 #pragma unroll
-    for (int i = 0; i < H; ++i) {
-        const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, r0 + i);
-#pragma unroll
-        for (int t = 0; t < NC; ++t) K[i][t] = load_cell(rs, voff + 32 * t);
-    }
+        for (int t = 0; t < NC; ++t) K[H - 1][t] = 0.f;
     bool asym = false;
-#pragma unroll
-    for (int t = 0; t < NC; ++t) {
-        const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, t);
+    stream_blocks([&](int c, const float *ch) {
         bool ne = false;
+        if (w == 0) {
+            if (c < H)
 #pragma unroll
-        for (int i = 0; i < H; ++i)
-            ne |= (r0 + i < rlim) & (__float_as_uint(load_cell(rs, toff + 32 * (r0 + i))) != __float_as_uint(K[i][t]));
-        asym |= (t < tlim) & ne;
-    }
+                for (int t = 0; t < NC; ++t) K[c][t] = ch[p * LDC + q + 8 * t];
+#pragma unroll
+            for (int a = 0; a < H; ++a)
+                if (a <= c) ne |= (a < rlim) & (__float_as_uint(ch[q * LDC + p + 8 * a]) != __float_as_uint(K[a][c]));
+        } else {
+            if (c >= H && c < 2 * H)
+#pragma unroll
+                for (int t = 0; t < NC; ++t) K[c - H][t] = ch[p * LDC + q + 8 * t];
+#pragma unroll
+            for (int a = H; a < 2 * H; ++a)
+                if (a <= c) ne |= (a < rlim) & (__float_as_uint(ch[q * LDC + p + 8 * a]) != __float_as_uint(K[a - H][c]));
+        }
+        asym |= (c < tlim) & ne;
+    });
     float mx = neg_inf(), mn = __builtin_inff();
     bool nan = false;
 #pragma unroll
@@ -296,7 +335,9 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     float err = ms > 0.f ? fabsf(U * X - ms) : 0.f, lsum;
     {
         // L_i = sum_j K_ij V_j C_ij with the cells reloaded (K is 0 off the
-        // problem, where the loaded cost is 0 or a finite neighbour).
+        // problem, where the loaded cost is 0 or a finite neighbour; a lane's
+        // cells of row block r at offset voff + 32 t from row 8r).
+        const int voff = (p * d + q) * 4;
         float l[H];
 #pragma unroll
         for (int i = 0; i < H; ++i) {
