@@ -19,8 +19,10 @@
 // transpose, so row i ends on one lane (p, q < H); S = K^T U takes U by rows
 // and sums its column partials over the lanes p and the two wavefronts
 // through LDS, so column j ends on thread j.  U lives on the row lanes, V on
-// the column threads; each is published to LDS for the next product.  Three
-// barriers per iteration (U published, column partials written, V published).
+// the column threads; each is published to LDS for the next product.  The
+// U a lane needs comes only from its own wavefront (the rows it holds), so
+// publishing U needs no barrier (a wavefront's LDS operations complete in
+// order); two barriers per iteration: column partials written, V published.
 #include "sk_device.h"
 #include "sk_internal.h"
 
@@ -169,8 +171,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
             for (int ii = 0; ii < H; ++ii) x[ii] = __builtin_fmaf(K[ii][t], wc[t], x[ii]);
         return row_totals<H>(x, tb, p, q);
     };
-    // Column partials of K^T u, u published by rows (column_total after a barrier).
+    // Column partials of K^T u, u published by rows by this wavefront's own
+    // lanes (column_total after a barrier).
     auto column_product = [&]() {
+        __builtin_amdgcn_wave_barrier();
         float wr[H];
 #pragma unroll
         for (int ii = 0; ii < H; ++ii) wr[ii] = rowv[p * kVS + 8 * w + ii];
@@ -218,7 +222,6 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
                 if (lane == 0) rd[w][0] = e;
             }
         }
-        __syncthreads();
         if (k == n_iter) break;
 
         column_product();
@@ -248,9 +251,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
     }
 
     // ---- the returned plan P = U K V, measured (Section 4): its marginals
-    // and sum_ij P_ij C_ij from the cost itself.  Nothing reads colv between
-    // the loop's last barrier and here. ----
-    if (c < 8 * N) colv[cslot] = V;
+    // and sum_ij P_ij C_ij from the cost itself.  colv holds the returned V
+    // unless the loop stopped early (then nothing has read it since the
+    // loop's last barrier). ----
+    if (kstop != n_iter && c < 8 * N) colv[cslot] = V;
     __syncthreads();
     if (ini[0][0] + ini[1][0] != 0.f) {
         if (threadIdx.x == 0) A.iters[b] = -1;
