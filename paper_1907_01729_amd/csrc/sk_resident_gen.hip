@@ -265,24 +265,26 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
         float wc[N];
 #pragma unroll
         for (int t = 0; t < N; ++t) wc[t] = colv[q * kVS + t];
-        // L_i = sum_j K_ij V_j C_ij with the cells reloaded (K is 0 off the
-        // problem, where the loaded cost is 0 or a finite neighbour).
+        // L_i = sum_j K_ij V_j C_ij with the cost recovered from K itself:
+        // on the cells of the problem log2 K = cl - clmax (the spread guard
+        // keeps K >= 2^-64), so L_i = -(sum_j K_ij V_j log2 K_ij + clmax R_i) / s
+        // -- no second read of the cost.  K is 0 off the problem (the select
+        // keeps 0 * log2 0 from becoming NaN).
         float x[H], l[H];
 #pragma unroll
         for (int ii = 0; ii < H; ++ii) {
-            const __amdgpu_buffer_rsrc_t rs = rows_rsrc(Cb, d1, d2, 8 * (w * H + ii));
             float xs = 0.f, ls = 0.f;
 #pragma unroll
             for (int t = 0; t < N; ++t) {
                 const float kv = K[ii][t] * wc[t];
                 xs += kv;
-                ls = __builtin_fmaf(kv, load_cell(rs, voff + 32 * t), ls);
+                ls = __builtin_fmaf(kv, kv > 0.f ? lg2(K[ii][t]) : 0.f, ls);
             }
             x[ii] = xs;
             l[ii] = ls;
         }
         const float R = row_totals<H>(x, tb, p, q);
-        const float L = row_totals<H>(l, tb, p, q);
+        const float L = -__builtin_fmaf(clmax, R, row_totals<H>(l, tb, p, q)) / s;
         err = ms > 0.f ? fabsf(U * R - ms) : 0.f;
         lsum = ms > 0.f ? U * L : 0.f;
     }

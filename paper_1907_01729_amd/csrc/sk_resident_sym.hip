@@ -56,16 +56,10 @@ __device__ __forceinline__ float kmul(const float (&K)[NR][NC], const float (&wc
     return row_totals<NR>(x, tb, p, q);
 }
 
-// Buffer descriptor over the d x d cost from row 8r on (reads past its end
-// return 0): a lane's column is the register offset, the row block an
-// immediate or a scalar offset.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t block_rsrc(const float *C, int d, int r) {
-    const int rest = d * d - 8 * r * d;
-    return __builtin_amdgcn_make_buffer_rsrc((void *)(C + (size_t)8 * r * d), (short)0, rest > 0 ? 4 * rest : 0,
-                                             0x00020000);
-}
-__device__ __forceinline__ float load_cell(__amdgpu_buffer_rsrc_t rsrc, int byte_off) {
-    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, byte_off, 0, 0));
+// Buffer descriptor over the d x d cost (reads past its end return 0): a
+// lane's column is the register offset, the row a scalar offset.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t cost_rsrc(const float *C, int d) {
+    return __builtin_amdgcn_make_buffer_rsrc((void *)C, (short)0, 4 * d * d, 0x00020000);
 }
 
 // Work-group = one problem, two wavefronts: wavefront w holds the row blocks
@@ -112,7 +106,7 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     constexpr int PF = NC < 4 ? NC : 4;  // row blocks in flight
     __shared__ __attribute__((aligned(16))) float cst[2][8 * LDC];
     const int tau = threadIdx.x;
-    const __amdgpu_buffer_rsrc_t whole = block_rsrc(A.C, d, 0);
+    const __amdgpu_buffer_rsrc_t whole = cost_rsrc(A.C, d);
     // Stream row blocks 0 .. NC-1 through LDS (PF in flight, one barrier per
     // block) and hand each staged block to visit(c, block).  Block c goes
     // into buffer c & 1, whose previous block was read before the last
@@ -334,21 +328,24 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     X = kmul<H, NC>(K, wc, tb, p, q);  // row sums R = K V
     float err = ms > 0.f ? fabsf(U * X - ms) : 0.f, lsum;
     {
-        // L_i = sum_j K_ij V_j C_ij with the cells reloaded (K is 0 off the
-        // problem, where the loaded cost is 0 or a finite neighbour; a lane's
-        // cells of row block r at offset voff + 32 t from row 8r).
-        const int voff = (p * d + q) * 4;
+        // L_i = sum_j K_ij V_j C_ij with the cost recovered from K itself:
+        // on the cells of the problem log2 K = cl - clmax (the spread guard
+        // keeps K >= 2^-64), so L_i = -(sum_j K_ij V_j log2 K_ij + clmax R_i) / s
+        // -- no second read of the cost.  Cells off the problem meet V = 0
+        // (the select keeps a K of 0 from turning 0 * log2 0 into NaN).
         float l[H];
 #pragma unroll
         for (int i = 0; i < H; ++i) {
-            const __amdgpu_buffer_rsrc_t rs = block_rsrc(A.C, d, r0 + i);
             float acc = 0.f;
 #pragma unroll
-            for (int t = 0; t < NC; ++t) acc = __builtin_fmaf(K[i][t] * wc[t], load_cell(rs, voff + 32 * t), acc);
+            for (int t = 0; t < NC; ++t) {
+                const float kv = K[i][t] * wc[t];
+                acc = __builtin_fmaf(kv, kv > 0.f ? lg2(K[i][t]) : 0.f, acc);
+            }
             l[i] = acc;
         }
         const float ls = row_totals<H>(l, tb, p, q);
-        lsum = ms > 0.f ? U * ls : 0.f;
+        lsum = ms > 0.f ? U * (-__builtin_fmaf(clmax, X, ls) / s) : 0.f;
     }
     gather_lds(xs[0]);
     X = kmul<H, NC>(K, wc, tb, p, q);  // column sums S = K^T U
