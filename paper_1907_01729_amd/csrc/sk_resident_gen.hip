@@ -157,11 +157,16 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
         return;
     }
 
+    // The FMAs of both products run at the lowest issue priority and the rest
+    // of the iteration at the highest: the wavefronts sharing a SIMD belong
+    // to different problems, and one problem's serial stretch (transposes,
+    // updates, exchanges) should not queue behind another's FMAs.
     // (K w)_i of the lane's row, w published by columns.
     auto row_product = [&]() -> float {
         float wc[N];
 #pragma unroll
         for (int t = 0; t < N; ++t) wc[t] = colv[q * kVS + t];
+        __builtin_amdgcn_s_setprio(0);
         float x[H];
 #pragma unroll
         for (int ii = 0; ii < H; ++ii) x[ii] = K[ii][0] * wc[0];
@@ -169,6 +174,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
         for (int t = 1; t < N; ++t)
 #pragma unroll
             for (int ii = 0; ii < H; ++ii) x[ii] = __builtin_fmaf(K[ii][t], wc[t], x[ii]);
+        __builtin_amdgcn_s_setprio(3);
         return row_totals<H>(x, tb, p, q);
     };
     // Column partials of K^T u, u published by rows by this wavefront's own
@@ -178,6 +184,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
         float wr[H];
 #pragma unroll
         for (int ii = 0; ii < H; ++ii) wr[ii] = rowv[p * kVS + 8 * w + ii];
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int t = 0; t < N; ++t) {
             float y = K[0][t] * wr[0];
@@ -185,6 +192,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void s
             for (int ii = 1; ii < H; ++ii) y = __builtin_fmaf(K[ii][t], wr[ii], y);
             cp[partial_at(w, p, q, t)] = y;
         }
+        __builtin_amdgcn_s_setprio(3);
     };
 
     const int n_iter = A.n_iter;

@@ -46,6 +46,11 @@ __device__ __forceinline__ bool scale_ok(float x) { return x >= kSMin && x <= kS
 // (K w) of the lane's row for the column-layout w (NR row blocks).
 template <int NR, int NC>
 __device__ __forceinline__ float kmul(const float (&K)[NR][NC], const float (&wc)[NC], float *tb, int p, int q) {
+    // The two wavefronts sharing a SIMD belong to different problems: the
+    // FMAs run at the lowest issue priority and the rest of the iteration
+    // (the transpose, the update, the exchange) at the highest, so that one
+    // problem's serial stretch is not queued behind the other's FMAs.
+    __builtin_amdgcn_s_setprio(0);
     float x[NR];
 #pragma unroll
     for (int r = 0; r < NR; ++r) x[r] = K[r][0] * wc[0];
@@ -53,6 +58,7 @@ __device__ __forceinline__ float kmul(const float (&K)[NR][NC], const float (&wc
     for (int t = 1; t < NC; ++t)
 #pragma unroll
         for (int r = 0; r < NR; ++r) x[r] = __builtin_fmaf(K[r][t], wc[t], x[r]);
+    __builtin_amdgcn_s_setprio(3);
     return row_totals<NR>(x, tb, p, q);
 }
 

@@ -159,6 +159,11 @@ __global__ __launch_bounds__(64 * kShWaves) __attribute__((amdgpu_waves_per_eu(2
             // One pass over the plan: row partials against the column half
             // of p, column partials against the row half (written out per
             // column block).
+            // (At the lowest issue priority: the wavefronts sharing a SIMD
+            // belong to different problems, and the serial rest of an
+            // iteration -- transposes, block sums -- should not queue
+            // behind another problem's FMAs.)
+            __builtin_amdgcn_s_setprio(0);
             float yr[H];
 #pragma unroll
             for (int ii = 0; ii < H; ++ii) yr[ii] = 0.f;
@@ -172,6 +177,7 @@ __global__ __launch_bounds__(64 * kShWaves) __attribute__((amdgpu_waves_per_eu(2
                 }
                 cp[0][partial_at(w, p, q, t)] = yc;
             }
+            __builtin_amdgcn_s_setprio(3);
             const float Pp = row_totals<H>(yr, tb, p, q);  // (P p_g)_i on the row owner
             __syncthreads();
             const float PTp = col_on ? column_total(cp[0], c) : 0.f;  // (P^T p_f)_j on the column owner
