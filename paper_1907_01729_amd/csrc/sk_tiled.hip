@@ -405,6 +405,7 @@ __device__ __forceinline__ void rows_step_points(const float (&ys)[NCW][D], cons
                                                  const float (&mui)[RB], const bool (&live)[RB], float *const (&a_row)[RB],
                                                  float (&colpart)[NCW], float &rowerr, float &losspart, int lane) {
     float xx[RB], e[RB][NCW], rs[RB];
+    __builtin_amdgcn_s_setprio(0);  // exponentials low, the row reductions high
 #pragma unroll
     for (int q = 0; q < RB; ++q) {
         xx[q] = sqnorm(xc[q]);
@@ -412,6 +413,7 @@ __device__ __forceinline__ void rows_step_points(const float (&ys)[NCW][D], cons
 #pragma unroll
         for (int c = 0; c < NCW; ++c) e[q][c] = live[q] ? ex2(dot2_from(xc[q], ys[c], bp[c]) + ax) : 0.f;
     }
+    __builtin_amdgcn_s_setprio(3);
 #pragma unroll
     for (int q = 0; q < RB; ++q) rs[q] = wave_sum(tree_sum<NCW>(e[q]));
     if (STATS) {
@@ -838,6 +840,10 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                     for (int c = 0; c < NCW; ++c) e[q][c] = cbuf[rq * D2P + 64 * c];
                 }
                 __builtin_amdgcn_sched_barrier(0);
+                // The exponentials at the lowest issue priority, the batch's
+                // serial reduction and update at the highest, so that another
+                // wavefront's exponentials fill this one's reduction latency.
+                __builtin_amdgcn_s_setprio(0);
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
                     ai[q] = uni(a_seg, rr0 + q);
@@ -845,6 +851,7 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                     for (int c = 0; c < NCW; ++c) e[q][c] = ex2(__builtin_fmaf(e[q][c], ns, ai[q] + bv[c]));
                     p[q] = tree_sum<NCW>(e[q]);
                 }
+                __builtin_amdgcn_s_setprio(3);
                 // Row updates of the batch, one row per 16-lane group (the
                 // all-reduce's packed layout): each lane fetches its row's
                 // potential and mass from the segment registers.
@@ -877,10 +884,12 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                     const float got = lane_get(upd ? an : av, lane_of_row<RB>(dq >= 0 && dq < RB ? dq : 0));
                     a_out = dq >= 0 && dq < RB ? got : a_out;
                 }
+                __builtin_amdgcn_s_setprio(0);
 #pragma unroll
                 for (int q = 0; q < RB; ++q)
 #pragma unroll
                     for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[q][c], f[q], colpart[c]);
+                __builtin_amdgcn_s_setprio(3);
                 if (!STATS && exact_any) {
 #pragma unroll
                     for (int q = 0; q < RB; ++q) {
