@@ -38,9 +38,9 @@ PEAK_FP32_VALU = 157.3
 # symmetric cost with d1 = d2 <= 104: the symmetric kernel; any other cost
 # (shared or per sample): the general kernel.
 RESIDENT_KERNELS = {
-    "sym": ("sk_resident_sym_kernel", "sk_resident_sym.hip", "alu", PEAK_FP32_VALU),
-    "shared": ("sk_resident_gen_kernel", "sk_resident_gen.hip", "alu", PEAK_FP32_VALU),
-    "batched": ("sk_resident_gen_kernel", "sk_resident_gen.hip", "alu", PEAK_FP32_VALU),
+    "sym": ("sk_resident_sym_kernel", ("sk_resident_sym.hip", "sk_resident_gen.h"), "alu", PEAK_FP32_VALU),
+    "shared": ("sk_resident_gen_kernel", ("sk_resident_gen.hip", "sk_resident_gen.h"), "alu", PEAK_FP32_VALU),
+    "batched": ("sk_resident_gen_kernel", ("sk_resident_gen.hip", "sk_resident_gen.h"), "alu", PEAK_FP32_VALU),
 }
 
 
@@ -265,7 +265,7 @@ def main():
         # only, on the stream the library launches on.  Algorithmic work: two
         # matrix-vector products (4*d1*d2 flops) per iteration, plus the first
         # v-update and the three products of the closing measurement (6*d1*d2).
-        kname, kfile, bound, peak = RESIDENT_KERNELS[resident_kind(prob)]
+        kname, kfiles, bound, peak = RESIDENT_KERNELS[resident_kind(prob)]
         os.environ["SK_RESIDENT_FORM"] = "plain"
         kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
         for k in range(args.steps):
@@ -279,7 +279,7 @@ def main():
         kernel_ms = float(np.mean([a.elapsed_time(b) for a, b in kev]))
         flops = float(np.sum(4.0 * iters + 6.0)) * prob.d1 * prob.d2
         achieved = flops / (kernel_ms * 1e-3) / 1e12
-        src = kernel_source_hash([kfile, "sk_device.h"])
+        src = kernel_source_hash([*kfiles, "sk_device.h"])
         traffic = stored_traffic(f"{kname}_{prob.name}_counters.md", src)
         roof = dict(bound=bound, achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                     frac=round(achieved / peak, 4), traffic=traffic, kernel=kname, kernel_ms=round(kernel_ms, 5),

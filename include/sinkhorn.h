@@ -86,17 +86,17 @@ SK_API size_t sinkhorn_workspace_bytes(const sk_problem *p);
  *
  * For max(d1, d2) <= 128 the same iterates are first computed in the plain
  * form of eq. (sk_plain), u = mu / (K v), v = nu / (K^T u), with K scaled by
- * its largest entry (a shared symmetric C with d1 = d2 <= 104: on the vector
- * ALU, K^T u = K u; any other C, shared or per sample: on the vector ALU with
- * K in registers); a problem whose scaled cost spans more than 64 bits, or
- * whose sums or scalings leave a guarded fp32 range at any iteration, is
+ * its largest entry, on the vector ALU with K in registers (a shared C with
+ * d1 = d2 <= 104 that proves symmetric: K^T u = K u; any other C, shared or
+ * per sample: both products); a problem whose scaled cost spans more than
+ * 64 bits, or whose sums or scalings leave a guarded fp32 range at any
+ * iteration, is
  * re-solved from the start by the log-domain kernel launched right after it
  * on the same stream.  Diagnostic switch (environment variable
  * SK_RESIDENT_FORM, read at every call): "log" runs the log-domain kernel
  * only; "plain" runs the first-choice plain-form kernel only, leaving the
- * problems it hands over with iters = -1 (out of range) or -2 (cost not
- * symmetric) and their other outputs unspecified; "nosym" skips the
- * symmetric-cost kernel.
+ * problems it hands over with iters = -1 (out of range) and their other
+ * outputs unspecified; "nosym" skips the symmetric-cost kernel.
  *
  *   mu        [B, d1]              input histograms
  *   nu        [B, d2]

@@ -26,7 +26,7 @@ sk_status check_problem(const sk_problem *p) {
 // Which resident kernels run (diagnostic switch, environment variable
 // SK_RESIDENT_FORM): "log" forces the log-domain kernel; "plain" runs the
 // first-choice plain-form kernel alone (problems it hands over stay at
-// iters = -1 or -2); "nosym" skips the symmetric-cost kernel; anything else
+// iters = -1); "nosym" skips the symmetric-cost kernel; anything else
 // runs the plain form with its fallbacks.
 constexpr int kFormAuto = 0, kFormLog = 1, kFormPlain = 2, kFormNoSym = 3;
 
@@ -61,23 +61,14 @@ sk::BwdArgs bwd_args(const sk_problem *p, const float *grad_loss, const float *m
 }
 
 // Resident regime.  First choice: the symmetric-cost kernel (shared cost,
-// d1 = d2 <= 104), else the general plain-form kernel (any cost).  Each
-// hands over what it cannot solve: the symmetric kernel to the general
-// kernel (iters = -2), both plain forms to the log-domain kernel
-// (iters = -1).  Launches on one stream, in order.
+// d1 = d2 <= 104; it runs the general iteration in place when the cost is
+// not symmetric), else the general plain-form kernel (any cost).  Either
+// hands the problems it cannot keep in range to the log-domain kernel
+// (iters = -1), launched next on the same stream.
 hipError_t launch_resident_regime(sk::FwdArgs a, int form, hipStream_t s) {
     if (form == kFormLog) return sk::launch_resident(a, s);
     hipError_t e = hipSuccess;
-    bool ran;
-    if (form != kFormNoSym && sk::launch_resident_sym(a, s, &e)) {
-        ran = true;
-        if (e == hipSuccess && form != kFormPlain) {
-            a.only_flagged = 2;
-            if (!sk::launch_resident_gen(a, s, &e)) return hipErrorInvalidValue;  // takes every shape the first takes
-        }
-    } else {
-        ran = sk::launch_resident_gen(a, s, &e);
-    }
+    const bool ran = (form != kFormNoSym && sk::launch_resident_sym(a, s, &e)) || sk::launch_resident_gen(a, s, &e);
     if (!ran) return sk::launch_resident(a, s);
     if (e != hipSuccess || form == kFormPlain) return e;
     a.only_flagged = 1;

@@ -18,9 +18,9 @@ struct FwdArgs {
     int B, d1, d2, n_iter, c_batched;
     float lambda, tol;
     float s;  // log2(e) / lambda
-    // Set when a plain-form launch ran first: solve only the problems it
-    // marked with iters = -only_flagged (-1: out of the plain form's range;
-    // -2: the cost is not symmetric) and leave the others untouched.
+    // Set (to 1) when a plain-form launch ran first: the log-domain kernel
+    // solves only the problems it marked with iters = -1 (out of the plain
+    // form's range) and leaves the others untouched.
     int only_flagged;
 };
 
@@ -41,12 +41,11 @@ hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
 // it does not take the shape; otherwise *err is the launch status.  Problems
 // it cannot keep in range come back with iters = -1.
 // A shared cost with d1 = d2 <= 104, two wavefronts per problem
-// on the vector ALU.  A cost that is not symmetric marks every problem with
-// iters = -2 (for the general kernel).
+// on the vector ALU.  On a cost that is not symmetric each work-group runs
+// the general kernel's iteration in place.
 bool launch_resident_sym(const FwdArgs &a, hipStream_t st, hipError_t *err);
 // Same contract; any cost (shared or per problem) with max(d1, d2) <= 128,
-// two wavefronts per problem on the vector ALU.  With only_flagged = 2 it
-// solves the problems marked iters = -2.
+// two wavefronts per problem on the vector ALU.
 bool launch_resident_gen(const FwdArgs &a, hipStream_t st, hipError_t *err);
 
 // The tiled sweep keeps a whole cost row in one wavefront's registers.

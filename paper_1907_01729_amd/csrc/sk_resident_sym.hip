@@ -22,26 +22,17 @@
 // passes.
 //
 // The kernel verifies the symmetry of the cost first, pair by pair (bit
-// equality); a cost that is not symmetric marks every problem with iters = -2
-// for the general kernel, launched next.  A problem outside the plain
+// equality); on a cost that is not symmetric every work-group runs the
+// general kernel's iteration in place (same outputs, same bits as that
+// kernel), so no second launch is needed.  A problem outside the plain
 // form's range gets iters = -1 (the log-domain kernel takes it): a cost
 // spread wider than the range at the start, or a guard that failed in any
 // iteration (checked once, at the end): a sum R_i, S_j outside
 // [2^-64, 2^64] or a scaling U_i, V_j outside [2^-100, 2^100] on the supports.
-#include "sk_device.h"
-#include "sk_internal.h"
+#include "sk_resident_gen.h"  // the general iteration, the range guards
 
 namespace sk {
 namespace {
-
-constexpr float kLo = 5.42101086242752217e-20f;   // 2^-64
-constexpr float kHi = 1.84467440737095516e19f;    // 2^64
-constexpr float kSMin = 7.8886090522101181e-31f;  // 2^-100
-constexpr float kSMax = 1.2676506002282294e30f;   // 2^100
-constexpr float kRangeBits = 64.f;
-
-__device__ __forceinline__ bool sum_ok(float x) { return x >= kLo && x <= kHi; }
-__device__ __forceinline__ bool scale_ok(float x) { return x >= kSMin && x <= kSMax; }
 
 // (K w) of the lane's row for the column-layout w (NR row blocks).
 template <int NR, int NC>
@@ -82,14 +73,24 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     // stride of 20 floats puts the 8 blocks q on distinct banks).
     constexpr int XS = 20;
     static_assert(2 * H <= XS, "row blocks per column-block line");
-    __shared__ __attribute__((aligned(16))) float xs[2][8 * XS];  // xs[0] = U, xs[1] = V
+    // Set-up staging of the cost: row stride LDC = 8 mod 64, so that row
+    // reads (p, q + 8t) and transposed reads (q, p + 8a) hit 64 banks.
+    constexpr int LDC = 136;
+    // One LDS pool, also the general iteration's when the cost proves not
+    // symmetric (the two never run at once): float offsets, 16-byte aligned.
+    constexpr int oXs = 0, oTsum = oXs + 2 * 8 * XS, oCst = oTsum + 2 * kRowTotalsFloats, oRed = oCst + 2 * 8 * LDC,
+                  oIni = oRed + 8, kSymLdsFloats = oIni + 16;
+    static_assert(oTsum % 4 == 0 && oCst % 4 == 0 && oRed % 4 == 0, "16-byte offsets");
+    __shared__ __attribute__((aligned(16))) float pool[kSymLdsFloats > kGenLdsFloats ? kSymLdsFloats : kGenLdsFloats];
+    float(&xs)[2][8 * XS] = lds_at<float[2][8 * XS]>(pool, oXs);  // xs[0] = U, xs[1] = V
     // Per-wavefront error reports of the stop test: [iteration parity]
     // [wavefront][row phase, column phase], one 16-byte read per decision.
     // The parity keeps a report readable until both wavefronts have passed
     // the next iteration's barriers.
-    __shared__ __attribute__((aligned(16))) float red[2][2][2];
-    __shared__ float ini[2][2][4];  // set-up exchanges
-    __shared__ __attribute__((aligned(16))) float tsum[2][kRowTotalsFloats];  // per-wavefront row-total scratch
+    float(&red)[2][2][2] = lds_at<float[2][2][2]>(pool, oRed);
+    float(&ini)[2][2][4] = lds_at<float[2][2][4]>(pool, oIni);  // set-up exchanges
+    float(&tsum)[2][kRowTotalsFloats] = lds_at<float[2][kRowTotalsFloats]>(pool, oTsum);  // per-wavefront row-total scratch
+    float(&cst)[2][8 * LDC] = lds_at<float[2][8 * LDC]>(pool, oCst);
 
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: descriptors stay scalar
@@ -108,9 +109,7 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     // then).  Cells off the problem are masked (row block r holds a row iff
     // r < rlim, column block t a column iff t < tlim).
     const int rlim = (d - p + 7) >> 3, tlim = (d - q + 7) >> 3;
-    constexpr int LDC = 136;             // = 8 mod 64: row reads (p, q + 8t) and transposed reads (q, p + 8a) hit 64 banks
     constexpr int PF = NC < 4 ? NC : 4;  // row blocks in flight
-    __shared__ __attribute__((aligned(16))) float cst[2][8 * LDC];
     const int tau = threadIdx.x;
     const __amdgpu_buffer_rsrc_t whole = cost_rsrc(A.C, d);
     // Stream row blocks 0 .. NC-1 through LDS (PF in flight, one barrier per
@@ -191,7 +190,8 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     }
     __syncthreads();
     if (ini[0][0][0] + ini[0][1][0] != 0.f) {  // the same verdict for every problem: the cost is shared
-        if (threadIdx.x == 0) A.iters[b] = -2;
+        __syncthreads();              // every thread has read the verdict: the pool is free
+        resident_gen_body<NC>(A, pool);  // the general iteration in place (its own reads of the cost)
         return;
     }
     // Raw cost range -> cl range (cl = -s C with s > 0: the extremes swap).
