@@ -10,8 +10,9 @@
 // potentials equal the log-domain iterates up to rounding.
 //
 // Lane l = p + 8q (p = l & 7, q = l >> 3) of wavefront w holds K[p + 8r][q + 8t]
-// for its row blocks r in [w H, w H + H) and every column block t < NC
-// (8 NC >= d, H = ceil(NC / 2)).  A product K w takes w "by columns"
+// for its row blocks (ceil(NC / 2) from 0 for w = 0, floor(NC / 2) after
+// them for w = 1) and every column block t < NC (8 NC >= d).  A product
+// K w takes w "by columns"
 // (register t of lane (p, q) holds w[q + 8t], read from LDS), forms per-lane
 // partial row sums over t, and sums them over the 8 lanes q through a small
 // per-wavefront LDS transpose: lane (p, q) writes its H partials, lane
@@ -59,29 +60,35 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t cost_rsrc(const float *C, int 
     return __builtin_amdgcn_make_buffer_rsrc((void *)C, (short)0, 4 * d * d, 0x00020000);
 }
 
-// Work-group = one problem, two wavefronts: wavefront w holds the row blocks
-// r in [w H, w H + H), H = ceil(NC / 2), against every column block, so each
-// computes whole row sums of its rows; the updated scalings meet in LDS (one
-// barrier per product).  Two wavefronts per problem put two per SIMD for a
-// batch of one problem per SIMD: a single wavefront issues a vector
-// instruction only every few cycles, two interleave.
-template <int NC>
-__global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
-    constexpr int H = (NC + 1) / 2;
-    // Column operand in LDS, by column block: row y at [y & 7][y >> 3], so
-    // that lane (p, q) reads its NC values contiguously (16-byte reads; a
-    // stride of 20 floats puts the 8 blocks q on distinct banks).
-    constexpr int XS = 20;
-    static_assert(2 * H <= XS, "row blocks per column-block line");
-    // Set-up staging of the cost: row stride LDC = 8 mod 64, so that row
-    // reads (p, q + 8t) and transposed reads (q, p + 8a) hit 64 banks.
-    constexpr int LDC = 136;
-    // One LDS pool, also the general iteration's when the cost proves not
-    // symmetric (the two never run at once): float offsets, 16-byte aligned.
-    constexpr int oXs = 0, oTsum = oXs + 2 * 8 * XS, oCst = oTsum + 2 * kRowTotalsFloats, oRed = oCst + 2 * 8 * LDC,
-                  oIni = oRed + 8, kSymLdsFloats = oIni + 16;
-    static_assert(oTsum % 4 == 0 && oCst % 4 == 0 && oRed % 4 == 0, "16-byte offsets");
-    __shared__ __attribute__((aligned(16))) float pool[kSymLdsFloats > kGenLdsFloats ? kSymLdsFloats : kGenLdsFloats];
+// Column operand in LDS, by column block: row y at [y & 7][y >> 3], so that
+// lane (p, q) reads its NC values contiguously (16-byte reads; a stride of
+// 20 floats puts the 8 blocks q on distinct banks).
+constexpr int XS = 20;
+// Set-up staging of the cost: row stride LDC = 8 mod 64, so that row reads
+// (p, q + 8t) and transposed reads (q, p + 8a) hit 64 banks.
+constexpr int LDC = 136;
+// One LDS pool, also the general iteration's when the cost proves not
+// symmetric (the two never run at once): float offsets, 16-byte aligned.
+constexpr int oXs = 0, oTsum = oXs + 2 * 8 * XS, oCst = oTsum + 2 * kRowTotalsFloats, oRed = oCst + 2 * 8 * LDC,
+              oIni = oRed + 8, kSymLdsFloats = oIni + 16;
+static_assert(oTsum % 4 == 0 && oCst % 4 == 0 && oRed % 4 == 0, "16-byte offsets");
+constexpr int kSymPoolFloats = kSymLdsFloats > kGenLdsFloats ? kSymLdsFloats : kGenLdsFloats;
+
+// Work-group = one problem, two wavefronts: wavefront W holds H row blocks
+// from R0 on (ceil(NC / 2) for the first, floor(NC / 2) for the second, so no
+// block lies past the problem) against every column block, so each computes
+// whole row sums of its rows; the updated scalings meet in LDS (one barrier
+// per product).  Two wavefronts per problem put two per SIMD for a batch of
+// one problem per SIMD: a single wavefront issues a vector instruction only
+// every few cycles, two interleave.  The two wavefronts run separate
+// instantiations (W = 0, 1) of this body, which pass the same barriers.
+// Returns true, for both wavefronts and after a barrier that frees the LDS
+// pool, when the cost is not symmetric (nothing written); false otherwise.
+template <int NC, int W>
+__device__ __forceinline__ bool sym_body(const FwdArgs &A, float *pool) {
+    constexpr int H = W == 0 ? (NC + 1) / 2 : NC / 2;
+    constexpr int R0 = W == 0 ? 0 : (NC + 1) / 2;
+    static_assert(R0 + H <= XS, "row blocks per column-block line");
     float(&xs)[2][8 * XS] = lds_at<float[2][8 * XS]>(pool, oXs);  // xs[0] = U, xs[1] = V
     // Per-wavefront error reports of the stop test: [iteration parity]
     // [wavefront][row phase, column phase], one 16-byte read per decision.
@@ -93,12 +100,12 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     float(&cst)[2][8 * LDC] = lds_at<float[2][8 * LDC]>(pool, oCst);
 
     const int lane = threadIdx.x & 63;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: descriptors stay scalar
+    constexpr int w = W;
     const int p = lane & 7, q = lane >> 3;
     const int b = blockIdx.x;
     const int d = A.d1;
     const float s = A.s;
-    const int r0 = w * H;  // first row block of this wavefront
+    constexpr int r0 = R0;  // first row block of this wavefront
 
     // Raw cost cells of the wavefront's row blocks and the symmetry check, the
     // cost streamed through LDS one row block (8 rows) at a time: thread tau
@@ -136,27 +143,15 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
         }
     };
     float K[H][NC];
-    if (2 * H > NC && w == 1)  // the padding row block past 8 NC rows is never staged
-#pragma unroll
-        for (int t = 0; t < NC; ++t) K[H - 1][t] = 0.f;
     bool asym = false;
     stream_blocks([&](int c, const float *ch) {
         bool ne = false;
-        if (w == 0) {
-            if (c < H)
+        if (c >= R0 && c < R0 + H)
 #pragma unroll
-                for (int t = 0; t < NC; ++t) K[c][t] = ch[p * LDC + q + 8 * t];
+            for (int t = 0; t < NC; ++t) K[c - R0][t] = ch[p * LDC + q + 8 * t];
 #pragma unroll
-            for (int a = 0; a < H; ++a)
-                if (a <= c) ne |= (a < rlim) & (__float_as_uint(ch[q * LDC + p + 8 * a]) != __float_as_uint(K[a][c]));
-        } else {
-            if (c >= H && c < 2 * H)
-#pragma unroll
-                for (int t = 0; t < NC; ++t) K[c - H][t] = ch[p * LDC + q + 8 * t];
-#pragma unroll
-            for (int a = H; a < 2 * H; ++a)
-                if (a <= c) ne |= (a < rlim) & (__float_as_uint(ch[q * LDC + p + 8 * a]) != __float_as_uint(K[a - H][c]));
-        }
+        for (int a = R0; a < R0 + H; ++a)
+            if (a <= c) ne |= (a < rlim) & (__float_as_uint(ch[q * LDC + p + 8 * a]) != __float_as_uint(K[a - R0][c]));
         asym |= (c < tlim) & ne;
     });
     float mx = neg_inf(), mn = __builtin_inff();
@@ -190,16 +185,15 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     }
     __syncthreads();
     if (ini[0][0][0] + ini[0][1][0] != 0.f) {  // the same verdict for every problem: the cost is shared
-        __syncthreads();              // every thread has read the verdict: the pool is free
-        resident_gen_body<NC>(A, pool);  // the general iteration in place (its own reads of the cost)
-        return;
+        __syncthreads();  // every thread has read the verdict: the pool is free
+        return true;
     }
     // Raw cost range -> cl range (cl = -s C with s > 0: the extremes swap).
     const float clmax = -s * fminf(ini[0][0][2], ini[0][1][2]);
     const float clmin = -s * fmaxf(ini[0][0][3], ini[0][1][3]);
     if (ini[0][0][1] + ini[0][1][1] != 0.f || !(clmax - clmin <= kRangeBits)) {  // a non-finite cost fails too
         if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+        return false;
     }
     // K on the cells of the problem; elsewhere a finite value in (0, 1]
     // (the clamp), which meets only zero operands and unused rows.
@@ -228,7 +222,7 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     __syncthreads();
     if (ini[1][0][0] + ini[1][1][0] == 0.f || ini[1][0][1] + ini[1][1][1] == 0.f) {  // empty support
         if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+        return false;
     }
 
     const int n_iter = A.n_iter;
@@ -328,7 +322,7 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     __syncthreads();
     if (ini[0][0][0] + ini[0][1][0] != 0.f) {
         if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+        return false;
     }
     gather_lds(xs[1]);
     X = kmul<H, NC>(K, wc, tb, p, q);  // row sums R = K V
@@ -372,6 +366,15 @@ __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
         A.marg_err[b] = red[0][0][0] + red[0][1][0];
         A.iters[b] = kstop;
     }
+    return false;
+}
+
+template <int NC>
+__global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
+    __shared__ __attribute__((aligned(16))) float pool[kSymPoolFloats];
+    const bool asym = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0 ? sym_body<NC, 0>(A, pool)
+                                                                            : sym_body<NC, 1>(A, pool);
+    if (asym) resident_gen_body<NC>(A, pool);  // the general iteration in place (its own reads of the cost)
 }
 
 template <int NC>
