@@ -605,3 +605,29 @@ def test_random_resident_problems(monkeypatch):
         _say(f"[random {case}]")
         gpu, ref = check_forward(prob)
         check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_random_asymmetric_shared_costs(monkeypatch):
+    """Twelve seeded shared square costs, symmetric but for one pair, over the
+    symmetric kernel's size buckets (d up to 104): each work-group finds the
+    pair and runs the general iteration in place.  Same bits as the general
+    kernel launched alone, and the oracle's results."""
+    rng = np.random.default_rng(4242)
+    for case, d in enumerate((2, 9, 16, 23, 40, 57, 64, 71, 90, 97, 100, 104)):
+        B = int(rng.integers(1, 9))
+        lam = float(10 ** rng.uniform(-1.3, 0.0))
+        n_iter = int(rng.integers(1, 120))
+        tol = float(rng.choice([0.0, 1e-5]))
+        prob = workloads.random_problem(seed=int(rng.integers(1 << 30)), B=B, d1=d, d2=d, lam=lam, n_iter=n_iter,
+                                        zero_frac=float(rng.choice([0.0, 0.2])), cost="sym", tol=tol)
+        i = int(rng.integers(0, d))
+        j = (i + 1 + int(rng.integers(0, d - 1))) % d  # j != i
+        prob.C[0, i, j] += 0.01
+        _say(f"[asym {case}] d={d} pair=({i},{j})")
+        monkeypatch.setenv("SK_RESIDENT_FORM", "nosym")
+        ref_bits = _gpu(prob)
+        monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+        gpu, ref = check_forward(prob)
+        for k in ("alpha", "beta", "loss", "marg_err", "iters"):
+            np.testing.assert_array_equal(gpu[k], ref_bits[k])
+        check_backward(prob, gpu, ref, grad_C=True)
