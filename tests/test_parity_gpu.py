@@ -631,3 +631,18 @@ def test_random_asymmetric_shared_costs(monkeypatch):
         for k in ("alpha", "beta", "loss", "marg_err", "iters"):
             np.testing.assert_array_equal(gpu[k], ref_bits[k])
         check_backward(prob, gpu, ref, grad_C=True)
+
+
+@pytest.mark.parametrize("form,c_batched", [("auto", False), ("nosym", False), ("log", False), ("auto", True)])
+def test_large_batch_resident(form, c_batched, monkeypatch):
+    """B = 70000 small problems (more than 65535 work-groups for the plain
+    kernels, problem indices past 16 bits) through each resident kernel; the
+    oracle checks samples on both sides of 65536."""
+    monkeypatch.setenv("SK_RESIDENT_FORM", form)
+    prob = workloads.random_problem(seed=77, B=70000, d1=8, d2=8, lam=0.1, n_iter=50, c_batched=c_batched,
+                                    cost="uniform" if c_batched else "sym")
+    gpu = _gpu(prob)
+    assert np.all(gpu["iters"] == 50)
+    idx = np.array([0, 1, 32767, 65535, 65536, 65537, 69998, 69999])
+    gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx, grad_C=c_batched)
