@@ -53,6 +53,9 @@ def test_regime_and_workspace_queries():
     assert sk.sinkhorn_workspace_bytes(4, 10, 10, 0, 0.1, 100) == 0
     assert sk.sinkhorn_workspace_bytes(256, 784, 784, 0, 0.01, 300) > 0
     assert sk.sinkhorn_regime(4, 200, 4097, 0) == 0  # no kernel takes d2 > 4096 beyond the resident sizes
+    assert sk.sinkhorn_regime(65535, 130, 130, 0) == 2  # the tiled regime's largest batch
+    assert sk.sinkhorn_regime(65536, 130, 130, 0) == 0
+    assert sk.sinkhorn_regime(1 << 20, 8, 8, 0) == 1  # the resident regime has no such limit
     assert sk.sinkhorn_workspace_bytes(-1, 784, 784, 0, 0.01, 300) == 0
 
 

@@ -646,3 +646,14 @@ def test_large_batch_resident(form, c_batched, monkeypatch):
     idx = np.array([0, 1, 32767, 65535, 65536, 65537, 69998, 69999])
     gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
     check_backward(prob, gpu, ref, idx=idx, grad_C=c_batched)
+
+
+def test_tiled_max_batch():
+    """The tiled regime's largest batch, B = 65535 (d = 130, shared cost):
+    every grid dimension at its limit; the oracle checks samples."""
+    prob = workloads.random_problem(seed=78, B=65535, d1=130, d2=130, lam=0.1, n_iter=20)
+    gpu = _gpu(prob)
+    assert np.all(gpu["iters"] == 20)
+    idx = np.array([0, 1, 7, 8, 32767, 65527, 65528, 65534])
+    gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx)
