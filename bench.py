@@ -183,7 +183,7 @@ def main():
                     help="only run a plain 256 MiB device copy 3 times (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (the batch is embarrassingly parallel; "
+        print("bench.py: measures one GPU only (the batch is embarrassingly parallel; "
               "multi-GPU sharding is design-only). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
