@@ -55,7 +55,9 @@ typedef enum {
     SK_ERR_LAMBDA = -3,    /* lambda not finite and > 0                       */
     SK_ERR_ITERS = -4,     /* n_iter < 0, or tol not finite                   */
     SK_ERR_WORKSPACE = -5, /* ws_bytes < sinkhorn_workspace_bytes(p)          */
-    SK_ERR_HIP = -6        /* a HIP launch failed (e.g. device is not gfx950) */
+    SK_ERR_HIP = -6,       /* a HIP launch failed (e.g. device is not gfx950) */
+    SK_ERR_ARG = -7        /* an argument outside its documented set of values
+                              (the selector of sinkhorn_forward_select)       */
 } sk_status;
 
 typedef struct {
@@ -90,13 +92,8 @@ SK_API size_t sinkhorn_workspace_bytes(const sk_problem *p);
  * d1 = d2 <= 104 that proves symmetric: K^T u = K u; any other C, shared or
  * per sample: both products); a problem whose scaled cost spans more than
  * 64 bits, or whose sums or scalings leave a guarded fp32 range at any
- * iteration, is
- * re-solved from the start by the log-domain kernel launched right after it
- * on the same stream.  Diagnostic switch (environment variable
- * SK_RESIDENT_FORM, read at every call): "log" runs the log-domain kernel
- * only; "plain" runs the first-choice plain-form kernel only, leaving the
- * problems it hands over with iters = -1 (out of range) and their other
- * outputs unspecified; "nosym" skips the symmetric-cost kernel.
+ * iteration, is re-solved from the start by the log-domain kernel launched
+ * right after it on the same stream.  Every problem is solved: iters >= 0.
  *
  *   mu        [B, d1]              input histograms
  *   nu        [B, d2]
@@ -116,6 +113,40 @@ SK_API sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const fl
                            const float *C, float *alpha, float *beta, float *loss,
                            float *marg_err, int32_t *iters, void *workspace,
                            size_t ws_bytes, void *stream);
+
+/*
+ * Diagnostic variant of sinkhorn_forward for tests and measurements: the
+ * same arguments, plus a selector that pins which kernels run.
+ *   SK_SELECT_DEFAULT        exactly sinkhorn_forward;
+ *   SK_SELECT_LOG_ONLY       resident shapes: the log-domain kernel alone
+ *                            (no plain-form attempt);
+ *   SK_SELECT_PLAIN_ONLY     resident shapes: the first-choice plain-form
+ *                            kernel alone, without the log-domain hand-over:
+ *                            a problem it cannot keep in range comes back
+ *                            with iters = -1 and its other outputs
+ *                            unspecified;
+ *   SK_SELECT_NO_SYMMETRIC   resident shapes: the general plain-form kernel
+ *                            even where the symmetric-cost kernel applies;
+ *   SK_SELECT_NO_COMPACTION  tiled shapes with a shared cost and tol > 0:
+ *                            stopped problems keep their sweep slots (the
+ *                            running batch is not compacted).
+ * Selectors that do not apply to the problem's regime change nothing.  Any
+ * other value: SK_ERR_ARG.  Results of the selectors other than
+ * SK_SELECT_PLAIN_ONLY equal those of sinkhorn_forward up to rounding (the
+ * same iterates); SK_SELECT_NO_COMPACTION gives identical bits.
+ */
+typedef enum {
+    SK_SELECT_DEFAULT = 0,
+    SK_SELECT_LOG_ONLY = 1,
+    SK_SELECT_PLAIN_ONLY = 2,
+    SK_SELECT_NO_SYMMETRIC = 3,
+    SK_SELECT_NO_COMPACTION = 4
+} sk_select;
+
+SK_API sk_status sinkhorn_forward_select(const sk_problem *p, int32_t select, const float *mu,
+                                         const float *nu, const float *C, float *alpha, float *beta,
+                                         float *loss, float *marg_err, int32_t *iters, void *workspace,
+                                         size_t ws_bytes, void *stream);
 
 /*
  * Backward (Section 2): the Lagrange-multiplier gradient of the entropic

@@ -18,6 +18,7 @@ from ._binding import (  # noqa: F401
     sinkhorn_backward_sharp,
     sinkhorn_forward,
     sinkhorn_forward_points,
+    sinkhorn_forward_select,
     sinkhorn_points_workspace_bytes,
     sinkhorn_regime,
     sinkhorn_status_string,
@@ -36,6 +37,7 @@ __all__ = [
     "sinkhorn_backward_sharp",
     "sinkhorn_forward",
     "sinkhorn_forward_points",
+    "sinkhorn_forward_select",
     "sinkhorn_loss",
     "sinkhorn_loss_points",
     "sinkhorn_points_workspace_bytes",

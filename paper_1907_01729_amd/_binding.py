@@ -1,6 +1,7 @@
 """ctypes binding of include/sinkhorn.h (argument marshalling only)."""
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -18,11 +19,16 @@ SK_STATUS = {
     -4: "SK_ERR_ITERS",
     -5: "SK_ERR_WORKSPACE",
     -6: "SK_ERR_HIP",
+    -7: "SK_ERR_ARG",
 }
+
+# Selector values of sinkhorn_forward_select (sk_select in include/sinkhorn.h).
+SK_SELECT = {"default": 0, "log": 1, "plain": 2, "nosym": 3, "nocompact": 4}
 
 EXPORTED = (
     "sinkhorn_workspace_bytes",
     "sinkhorn_forward",
+    "sinkhorn_forward_select",
     "sinkhorn_backward",
     "sinkhorn_status_string",
     "sinkhorn_regime",
@@ -71,6 +77,8 @@ def load_library():
     lib.sinkhorn_workspace_bytes.restype = ctypes.c_size_t
     lib.sinkhorn_forward.argtypes = [PP, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     lib.sinkhorn_forward.restype = ctypes.c_int
+    lib.sinkhorn_forward_select.argtypes = [PP, ctypes.c_int32, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.sinkhorn_forward_select.restype = ctypes.c_int
     lib.sinkhorn_backward.argtypes = [PP, P, P, P, P, P, P, P, P, P, P]
     lib.sinkhorn_backward.restype = ctypes.c_int
     lib.sinkhorn_status_string.argtypes = [ctypes.c_int]
@@ -140,32 +148,53 @@ def _stream(device, stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def sinkhorn_forward(mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None):
-    """Run the forward on the GPU.
+def _on(stream):
+    """Context in which outputs and the workspace are allocated: the stream the
+    library will run on, so that PyTorch's caching allocator orders their reuse
+    after the library's kernels (a temporary workspace is freed on return,
+    while the kernels may still be using it)."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
 
-    mu [B,d1], nu [B,d2], C [d1,d2] | [1,d1,d2] | [B,d1,d2]: float32 CUDA tensors.
-    Returns dict(alpha [B,d1], beta [B,d2], loss [B], marg_err [B], iters [B] int32).
-    """
+
+def _forward(select, mu, nu, C, lam, n_iter, tol, stream, workspace):
     lib = load_library()
     _dev(mu, "mu"), _dev(nu, "nu"), _dev(C, "C")
     B, d1, d2, cb = _shapes(mu, nu, C)
     p = problem(B, d1, d2, cb, lam, n_iter, tol)
     dev = mu.device
     f = dict(device=dev, dtype=torch.float32)
-    alpha = torch.empty((B, d1), **f)
-    beta = torch.empty((B, d2), **f)
-    loss = torch.empty((B,), **f)
-    merr = torch.empty((B,), **f)
-    iters = torch.empty((B,), device=dev, dtype=torch.int32)
-    need = int(lib.sinkhorn_workspace_bytes(ctypes.byref(p)))
-    if workspace is None or workspace.numel() < need:
-        workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
-    st = lib.sinkhorn_forward(ctypes.byref(p), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha), _ptr(beta), _ptr(loss),
-                              _ptr(merr), _ptr(iters), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
-                              _stream(dev, stream))
+    with _on(stream):
+        alpha = torch.empty((B, d1), **f)
+        beta = torch.empty((B, d2), **f)
+        loss = torch.empty((B,), **f)
+        merr = torch.empty((B,), **f)
+        iters = torch.empty((B,), device=dev, dtype=torch.int32)
+        need = int(lib.sinkhorn_workspace_bytes(ctypes.byref(p)))
+        if workspace is None or workspace.numel() < need:
+            workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
+    st = lib.sinkhorn_forward_select(ctypes.byref(p), int(select), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
+                                     _ptr(beta), _ptr(loss), _ptr(merr), _ptr(iters), _ptr(workspace),
+                                     ctypes.c_size_t(workspace.numel()), _stream(dev, stream))
     if st != 0:
-        raise SinkhornError(st, "sinkhorn_forward")
+        raise SinkhornError(st, "sinkhorn_forward" if select == 0 else "sinkhorn_forward_select")
     return dict(alpha=alpha, beta=beta, loss=loss, marg_err=merr, iters=iters)
+
+
+def sinkhorn_forward(mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None):
+    """Run the forward on the GPU.
+
+    mu [B,d1], nu [B,d2], C [d1,d2] | [1,d1,d2] | [B,d1,d2]: float32 CUDA tensors.
+    Returns dict(alpha [B,d1], beta [B,d2], loss [B], marg_err [B], iters [B] int32).
+    """
+    return _forward(0, mu, nu, C, lam, n_iter, tol, stream, workspace)
+
+
+def sinkhorn_forward_select(select, mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None):
+    """Diagnostic forward with pinned kernels: select is one of "default",
+    "log", "plain", "nosym", "nocompact" (see sk_select in sinkhorn.h)."""
+    if select not in SK_SELECT:
+        raise ValueError(f"select must be one of {sorted(SK_SELECT)}, got {select!r}")
+    return _forward(SK_SELECT[select], mu, nu, C, lam, n_iter, tol, stream, workspace)
 
 
 def sinkhorn_backward(grad_loss, mu, nu, C, lam, alpha, beta, grad_C=False, stream=None):
@@ -177,9 +206,10 @@ def sinkhorn_backward(grad_loss, mu, nu, C, lam, alpha, beta, grad_C=False, stre
     p = problem(B, d1, d2, cb, lam, 0, 0.0)
     dev = mu.device
     f = dict(device=dev, dtype=torch.float32)
-    gmu = torch.empty((B, d1), **f)
-    gnu = torch.empty((B, d2), **f)
-    gC = torch.empty(((B if cb else 1), d1, d2), **f) if grad_C else None
+    with _on(stream):
+        gmu = torch.empty((B, d1), **f)
+        gnu = torch.empty((B, d2), **f)
+        gC = torch.empty(((B if cb else 1), d1, d2), **f) if grad_C else None
     st = lib.sinkhorn_backward(ctypes.byref(p), _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
                                _ptr(beta), _ptr(gmu), _ptr(gnu), _ptr(gC), _stream(dev, stream))
     if st != 0:
@@ -225,14 +255,15 @@ def sinkhorn_forward_points(mu, nu, X, Y, lam, n_iter, tol=0.0, stream=None, wor
     p = problem(B, d1, d2, cb, lam, n_iter, tol)
     dev = mu.device
     f = dict(device=dev, dtype=torch.float32)
-    alpha = torch.empty((B, d1), **f)
-    beta = torch.empty((B, d2), **f)
-    loss = torch.empty((B,), **f)
-    merr = torch.empty((B,), **f)
-    iters = torch.empty((B,), device=dev, dtype=torch.int32)
-    need = int(lib.sinkhorn_points_workspace_bytes(ctypes.byref(p), D))
-    if workspace is None or workspace.numel() < need:
-        workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
+    with _on(stream):
+        alpha = torch.empty((B, d1), **f)
+        beta = torch.empty((B, d2), **f)
+        loss = torch.empty((B,), **f)
+        merr = torch.empty((B,), **f)
+        iters = torch.empty((B,), device=dev, dtype=torch.int32)
+        need = int(lib.sinkhorn_points_workspace_bytes(ctypes.byref(p), D))
+        if workspace is None or workspace.numel() < need:
+            workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
     st = lib.sinkhorn_forward_points(ctypes.byref(p), D, _ptr(mu), _ptr(nu), _ptr(X), _ptr(Y), _ptr(alpha),
                                      _ptr(beta), _ptr(loss), _ptr(merr), _ptr(iters), _ptr(workspace),
                                      ctypes.c_size_t(workspace.numel()), _stream(dev, stream))
@@ -251,10 +282,11 @@ def sinkhorn_backward_points(grad_loss, mu, nu, X, Y, lam, alpha, beta, grad_poi
     p = problem(B, d1, d2, cb, lam, 0, 0.0)
     dev = mu.device
     f = dict(device=dev, dtype=torch.float32)
-    gmu = torch.empty((B, d1), **f)
-    gnu = torch.empty((B, d2), **f)
-    gX = torch.empty(X.shape, **f) if grad_points else None
-    gY = torch.empty(Y.shape, **f) if grad_points else None
+    with _on(stream):
+        gmu = torch.empty((B, d1), **f)
+        gnu = torch.empty((B, d2), **f)
+        gX = torch.empty(X.shape, **f) if grad_points else None
+        gY = torch.empty(Y.shape, **f) if grad_points else None
     st = lib.sinkhorn_backward_points(ctypes.byref(p), D, _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(X), _ptr(Y),
                                       _ptr(alpha), _ptr(beta), _ptr(gmu), _ptr(gnu), _ptr(gX), _ptr(gY),
                                       _stream(dev, stream))
@@ -277,9 +309,10 @@ def sinkhorn_backward_sharp(grad_loss, mu, nu, C, lam, alpha, beta, max_cg=200, 
     p = problem(B, d1, d2, cb, lam, 0, 0.0)
     dev = mu.device
     f = dict(device=dev, dtype=torch.float32)
-    gmu = torch.empty((B, d1), **f)
-    gnu = torch.empty((B, d2), **f)
-    its = torch.empty((B,), device=dev, dtype=torch.int32)
+    with _on(stream):
+        gmu = torch.empty((B, d1), **f)
+        gnu = torch.empty((B, d2), **f)
+        its = torch.empty((B,), device=dev, dtype=torch.int32)
     st = lib.sinkhorn_backward_sharp(ctypes.byref(p), _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
                                      _ptr(beta), _ptr(gmu), _ptr(gnu), int(max_cg), ctypes.c_float(cg_tol),
                                      _ptr(its), _stream(dev, stream))

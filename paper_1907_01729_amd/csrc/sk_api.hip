@@ -2,8 +2,6 @@
 // regime dispatch and launches.  No allocation, no synchronisation.
 #include <math.h>
 #include <stdint.h>
-#include <stdlib.h>
-#include <string.h>
 
 #include "sk_internal.h"
 
@@ -21,22 +19,6 @@ sk_status check_problem(const sk_problem *p) {
     if (!(p->lambda > 0.f) || !isfinite(p->lambda)) return SK_ERR_LAMBDA;
     if (p->n_iter < 0 || !isfinite(p->tol)) return SK_ERR_ITERS;
     return SK_OK;
-}
-
-// Which resident kernels run (diagnostic switch, environment variable
-// SK_RESIDENT_FORM): "log" forces the log-domain kernel; "plain" runs the
-// first-choice plain-form kernel alone (problems it hands over stay at
-// iters = -1); "nosym" skips the symmetric-cost kernel; anything else
-// runs the plain form with its fallbacks.
-constexpr int kFormAuto = 0, kFormLog = 1, kFormPlain = 2, kFormNoSym = 3;
-
-int resident_form() {
-    const char *e = getenv("SK_RESIDENT_FORM");
-    if (!e) return kFormAuto;
-    if (!strcmp(e, "log")) return kFormLog;
-    if (!strcmp(e, "plain")) return kFormPlain;
-    if (!strcmp(e, "nosym")) return kFormNoSym;
-    return kFormAuto;
 }
 
 sk::BwdArgs bwd_args(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu, const float *C,
@@ -64,13 +46,15 @@ sk::BwdArgs bwd_args(const sk_problem *p, const float *grad_loss, const float *m
 // d1 = d2 <= 104; it runs the general iteration in place when the cost is
 // not symmetric), else the general plain-form kernel (any cost).  Either
 // hands the problems it cannot keep in range to the log-domain kernel
-// (iters = -1), launched next on the same stream.
-hipError_t launch_resident_regime(sk::FwdArgs a, int form, hipStream_t s) {
-    if (form == kFormLog) return sk::launch_resident(a, s);
+// (iters = -1), launched next on the same stream.  The selector of
+// sinkhorn_forward_select can pin one of these kernels.
+hipError_t launch_resident_regime(sk::FwdArgs a, hipStream_t s) {
+    if (a.select == SK_SELECT_LOG_ONLY) return sk::launch_resident(a, s);
     hipError_t e = hipSuccess;
-    const bool ran = (form != kFormNoSym && sk::launch_resident_sym(a, s, &e)) || sk::launch_resident_gen(a, s, &e);
+    const bool ran = (a.select != SK_SELECT_NO_SYMMETRIC && sk::launch_resident_sym(a, s, &e)) ||
+                     sk::launch_resident_gen(a, s, &e);
     if (!ran) return sk::launch_resident(a, s);
-    if (e != hipSuccess || form == kFormPlain) return e;
+    if (e != hipSuccess || a.select == SK_SELECT_PLAIN_ONLY) return e;
     a.only_flagged = 1;
     return sk::launch_resident(a, s);
 }
@@ -95,6 +79,7 @@ sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, cons
     a.tol = p->tol;
     a.s = sk::kLog2eHost / p->lambda;
     a.only_flagged = 0;
+    a.select = SK_SELECT_DEFAULT;
     return a;
 }
 
@@ -102,7 +87,7 @@ sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, cons
 // resident kernels with their hand-overs).
 hipError_t run_forward(const sk::FwdArgs &a, void *workspace, hipStream_t s) {
     if (!sk::resident_fits(a.d1, a.d2)) return sk::launch_tiled(a, workspace, s);
-    return launch_resident_regime(a, resident_form(), s);
+    return launch_resident_regime(a, s);
 }
 
 // ---- point clouds ----
@@ -142,6 +127,7 @@ const char *sinkhorn_status_string(sk_status s) {
         case SK_ERR_ITERS: return "n_iter must be >= 0 and tol finite";
         case SK_ERR_WORKSPACE: return "workspace smaller than sinkhorn_workspace_bytes()";
         case SK_ERR_HIP: return "HIP launch failed (is the device a gfx950?)";
+        case SK_ERR_ARG: return "an argument is outside its documented set of values";
     }
     return "unknown status";
 }
@@ -163,9 +149,10 @@ size_t sinkhorn_workspace_bytes(const sk_problem *p) {
     return sk::tiled_workspace_bytes(p->B, p->d1, p->d2, p->c_batched);
 }
 
-sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu, const float *C, float *alpha,
-                           float *beta, float *loss, float *marg_err, int32_t *iters, void *workspace,
-                           size_t ws_bytes, void *stream) {
+sk_status sinkhorn_forward_select(const sk_problem *p, int32_t select, const float *mu, const float *nu,
+                                  const float *C, float *alpha, float *beta, float *loss, float *marg_err,
+                                  int32_t *iters, void *workspace, size_t ws_bytes, void *stream) {
+    if (select < SK_SELECT_DEFAULT || select > SK_SELECT_NO_COMPACTION) return SK_ERR_ARG;
     sk_status st = check_problem(p);
     if (st != SK_OK) return st;
     if (p->B == 0) return SK_OK;
@@ -173,8 +160,16 @@ sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu
     const size_t need = sinkhorn_workspace_bytes(p);
     if (ws_bytes < need) return SK_ERR_WORKSPACE;
     if (need > 0 && !workspace) return SK_ERR_NULLPTR;
-    const sk::FwdArgs a = fwd_args(p, mu, nu, C, alpha, beta, loss, marg_err, iters);
+    sk::FwdArgs a = fwd_args(p, mu, nu, C, alpha, beta, loss, marg_err, iters);
+    a.select = select;
     return run_forward(a, workspace, static_cast<hipStream_t>(stream)) == hipSuccess ? SK_OK : SK_ERR_HIP;
+}
+
+sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu, const float *C, float *alpha,
+                           float *beta, float *loss, float *marg_err, int32_t *iters, void *workspace,
+                           size_t ws_bytes, void *stream) {
+    return sinkhorn_forward_select(p, SK_SELECT_DEFAULT, mu, nu, C, alpha, beta, loss, marg_err, iters, workspace,
+                                   ws_bytes, stream);
 }
 
 sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu,

@@ -85,19 +85,21 @@ __global__ __launch_bounds__(kBwdThreads) void sk_bwd_gradC_batched(BwdArgs A) {
 }
 
 // Shared C: grad_C[i, j] = sum_b g_b P_b[i, j]; one thread per (i, j), the
-// batch summed in order b = 0..B-1.
+// batch summed in order b = 0..B-1.  Rows are grid-strided over grid y, so any
+// d1 fits the grid.
 __global__ __launch_bounds__(kBwdThreads) void sk_bwd_gradC_shared(BwdArgs A) {
-    const int i = blockIdx.y;
     const int j = blockIdx.x * kBwdThreads + threadIdx.x;
     if (j >= A.d2) return;
-    const float c = -A.s * A.C[(size_t)i * A.d2 + j];
-    float acc = 0.f;
-    for (int b = 0; b < A.B; ++b) {
-        const float ai = A.alpha[(size_t)b * A.d1 + i] * kLog2e;
-        const float x = __builtin_fmaf(A.beta[(size_t)b * A.d2 + j], kLog2e, ai) + c;
-        acc = __builtin_fmaf(A.grad_loss[b], ex2(x), acc);
+    for (int i = blockIdx.y; i < A.d1; i += gridDim.y) {
+        const float c = -A.s * A.C[(size_t)i * A.d2 + j];
+        float acc = 0.f;
+        for (int b = 0; b < A.B; ++b) {
+            const float ai = A.alpha[(size_t)b * A.d1 + i] * kLog2e;
+            const float x = __builtin_fmaf(A.beta[(size_t)b * A.d2 + j], kLog2e, ai) + c;
+            acc = __builtin_fmaf(A.grad_loss[b], ex2(x), acc);
+        }
+        A.grad_C[(size_t)i * A.d2 + j] = acc;
     }
-    A.grad_C[(size_t)i * A.d2 + j] = acc;
 }
 
 }  // namespace
@@ -115,7 +117,7 @@ hipError_t launch_backward(const BwdArgs &a, hipStream_t st) {
             else
                 hipLaunchKernelGGL(sk_bwd_gradC_batched<false>, dim3(blocks), dim3(kBwdThreads), 0, st, a);
         } else {
-            dim3 grid((a.d2 + kBwdThreads - 1) / kBwdThreads, a.d1);
+            dim3 grid((a.d2 + kBwdThreads - 1) / kBwdThreads, a.d1 < 65535 ? a.d1 : 65535);
             hipLaunchKernelGGL(sk_bwd_gradC_shared, grid, dim3(kBwdThreads), 0, st, a);
         }
     }

@@ -22,6 +22,8 @@ struct FwdArgs {
     // solves only the problems it marked with iters = -1 (out of the plain
     // form's range) and leaves the others untouched.
     int only_flagged;
+    // Kernel selector of sinkhorn_forward_select (an sk_select value).
+    int select;
 };
 
 struct BwdArgs {

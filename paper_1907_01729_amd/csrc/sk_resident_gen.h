@@ -157,7 +157,7 @@ __device__ __forceinline__ void resident_gen_body(const FwdArgs &A, float *pool)
     for (int ii = 0; ii < H; ++ii)
 #pragma unroll
         for (int t = 0; t < N; ++t)
-            K[ii][t] = (w * H + ii < rlim) & (t < tlim) ? ex2(fminf(-s * K[ii][t] - clmax, 0.f)) : 0.f;
+            K[ii][t] = ((w * H + ii < rlim) && (t < tlim)) ? ex2(fminf(-s * K[ii][t] - clmax, 0.f)) : 0.f;
 
     // Owners: lane (p, q < H) owns row i = p + 8 (w H + q); thread c owns
     // column c.  Marginals are 0 off the problem.

@@ -26,9 +26,6 @@
 // the same decision, and the first row block records K = k in the stop flag,
 // which later sweeps and merges honour.  Row-error partials are double
 // buffered so a decision never reads a partial being rewritten.
-#include <stdlib.h>
-#include <string.h>
-
 #include "sk_device.h"
 #include "sk_internal.h"
 
@@ -57,11 +54,13 @@ struct TiledArgs {
     float *part;     // [2][R][B, d2p] column partials (plane 1 only for the exact pass)
     float *rowerr;   // [3][R][B] row-error partials: planes 0/1 by iteration parity, 2 for stats
     float *lossp;    // [R][B] loss partials (stats)
-    float *colerr;   // [B][JC] column-error partials of the merge
     int32_t *state;  // [B] 0 = running, K > 0 = stopped after iteration K
+    // Early stop with a compacted batch: sync[0] counts the problems stopped
+    // since the running list was last rebuilt.
+    int32_t *sync;
     // Compaction of the shared-cost sweep's batch (early stop only; else
-    // null): order[0, nlive) lists the running problems in increasing order,
-    // rebuilt by sk_tiled_compact before every sweep k >= 2.
+    // null): order[0, nlive) lists the running problems in increasing order;
+    // the identity at first, rebuilt by the merge after a problem stops.
     int32_t *order, *nlive;
     float *alpha_out, *beta_out, *loss_out, *merr_out;
     int32_t *iters_out;
@@ -75,17 +74,19 @@ __device__ __forceinline__ size_t pidx(const TiledArgs &T, int plane, int r, int
     return (((size_t)plane * T.R + r) * T.B + b) * (size_t)T.d2p + j;
 }
 
-// Work-group sum in a fixed order (deterministic); `red` holds kWaves floats.
-__device__ __forceinline__ float block_sum(float v, float *red) {
+// Work-group sum in a fixed order (deterministic); `red` holds NT/64 floats.
+template <int NT>
+__device__ __forceinline__ float block_sum_n(float v, float *red) {
     v = wave_sum(v);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
     __syncthreads();
     float s = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) s += red[w];
+    for (int w = 0; w < NT / 64; ++w) s += red[w];
     return s;
 }
+__device__ __forceinline__ float block_sum(float v, float *red) { return block_sum_n<kThreads>(v, red); }
 
 __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
     const size_t n = (size_t)T.B * T.d1;
@@ -100,8 +101,14 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
         if (row < (size_t)T.B && j < T.d2 && !(T.nu[row * T.d2 + j] > 0.f)) v = neg_inf();
         T.bbuf[u] = v;
     }
-    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < (size_t)T.B; u += (size_t)gridDim.x * kThreads)
+    for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < (size_t)T.B; u += (size_t)gridDim.x * kThreads) {
         T.state[u] = 0;
+        if (T.order) T.order[u] = (int32_t)u;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        T.sync[0] = 0;
+        if (T.nlive) *T.nlive = T.B;
+    }
 }
 
 // Scaled cost of one cell from the point clouds, in the centred expansion
@@ -174,50 +181,118 @@ __device__ float col_lse_exact(const TiledArgs &T, int b, int j) {
     return m + lg2(s);
 }
 
-// Merge of the row blocks' column partials (fixed order) and v-update.
-// EXACT: partials are (max, sumexp) pairs of the first v-update.
-// Otherwise: partials are the column sums of the plan after sweep k; this also
-// yields the column part of iterate k's marginal error.
-template <bool EXACT>
-__global__ __launch_bounds__(kMergeThreads) void sk_tiled_merge(TiledArgs T, int k) {
+// Merge of the row blocks' (max, sumexp) partials of the first v-update
+// (fixed order): beta of iteration 1.
+__global__ __launch_bounds__(kMergeThreads) void sk_tiled_merge_exact(TiledArgs T) {
     const int j = blockIdx.x * kMergeThreads + threadIdx.x;
     const int b = blockIdx.y;
-    if (!EXACT && T.state[b] != 0) return;  // block-uniform
-    float err = 0.f;
-    if (j < T.d2) {
-        const float nuj = T.nu[(size_t)b * T.d2 + j];
-        float bnew = neg_inf();
-        if (EXACT) {
-            float M = kNegBig;
-            for (int r = 0; r < T.R; ++r) M = fmaxf(M, T.part[pidx(T, 0, r, b, j)]);
-            float S = 0.f;
-            for (int r = 0; r < T.R; ++r) S += T.part[pidx(T, 1, r, b, j)] * ex2(T.part[pidx(T, 0, r, b, j)] - M);
-            if (nuj > 0.f) bnew = log2f(nuj) - (M + lg2(S));
-            T.bbuf[(size_t)1 * T.B * T.d2p + (size_t)b * T.d2p + j] = bnew;
-        } else {
-            // Fixed-order sum over the row blocks; 8 loads in flight at a time.
-            float cs = 0.f;
-            for (int r0 = 0; r0 < T.R; r0 += 8) {
-                float v[8];
+    if (j >= T.d2) return;
+    const float nuj = T.nu[(size_t)b * T.d2 + j];
+    float bnew = neg_inf();
+    float M = kNegBig;
+    for (int r = 0; r < T.R; ++r) M = fmaxf(M, T.part[pidx(T, 0, r, b, j)]);
+    float S = 0.f;
+    for (int r = 0; r < T.R; ++r) S += T.part[pidx(T, 1, r, b, j)] * ex2(T.part[pidx(T, 0, r, b, j)] - M);
+    if (nuj > 0.f) bnew = log2f(nuj) - (M + lg2(S));
+    T.bbuf[(size_t)1 * T.B * T.d2p + (size_t)b * T.d2p + j] = bnew;
+}
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// Running list of a compacted batch: order[0, nlive) = the problems with
+// state 0, increasing (one work-group of NT threads, ballot prefix sums).  It
+// runs beside the merges of the same launch, so a problem those merges stop
+// may or may not be listed yet; the sweep skips stopped problems either way,
+// and which slot a problem takes never changes its bits.
+template <int NT>
+__device__ void relist_running(const TiledArgs &T) {
+    __shared__ int wsum[NT / 64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int base = 0;
+    for (int b0 = 0; b0 < T.B; b0 += NT) {
+        const int b = b0 + threadIdx.x;
+        const bool live = b < T.B && T.state[b] == 0;
+        const unsigned long long m = __ballot(live);
+        if (lane == 0) wsum[w] = __popcll(m);
+        __syncthreads();
+        int off = base, tot = 0;
 #pragma unroll
-                for (int q = 0; q < 8; ++q) v[q] = r0 + q < T.R ? T.part[pidx(T, 0, r0 + q, b, j)] : 0.f;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) cs += v[q];
-            }
-            err = fabsf(cs - nuj);
-            if (nuj > 0.f) {
-                const float bold = T.bbuf[(size_t)(k & 1) * T.B * T.d2p + (size_t)b * T.d2p + j];
-                if (cs >= kSumLo && cs <= kSumHi)
-                    bnew = bold + log2f(nuj) - lg2(cs);
-                else
-                    bnew = log2f(nuj) - col_lse_exact(T, b, j);
-            }
-            T.bbuf[(size_t)((k + 1) & 1) * T.B * T.d2p + (size_t)b * T.d2p + j] = bnew;
+        for (int q = 0; q < NT / 64; ++q) {
+            off += q < w ? wsum[q] : 0;
+            tot += wsum[q];
         }
+        if (live) T.order[off + __popcll(m & ((1ull << lane) - 1ull))] = b;
+        base += tot;
+        __syncthreads();
     }
-    if (!EXACT) {
-        err = wave_sum(err);
-        if (threadIdx.x == 0) T.colerr[(size_t)b * T.JC + blockIdx.x] = err;
+    if (threadIdx.x == 0) *T.nlive = base;
+}
+
+// Merge after sweep k (k < n_iter), one work-group per problem: column sums
+// of the plan after the u-update of iteration k, summed over the row blocks in
+// a fixed order; the v-update of iteration k+1; iterate k's marginal error.
+// Each thread takes groups of four consecutive columns (16-byte loads of the
+// padded rows; padding columns keep 0).
+//
+// Early stop (tol > 0): the work-group holds problem b's whole error (column
+// part summed here, row part from the sweep's row-block partials), so it stops
+// b at K = k when the error is <= tol without any exchange with other
+// work-groups; every later launch skips b.  With a compacted batch, stops are
+// counted in sync[0], and one extra work-group (index B) rebuilds the running
+// list from the stops of earlier launches when the count is nonzero.
+template <int NT>
+__global__ __launch_bounds__(NT) void sk_tiled_merge_cols(TiledArgs T, int k) {
+    __shared__ float red[NT / 64];
+    const int b = blockIdx.x;
+    if (b == T.B) {  // the relist work-group of a compacted batch
+        const int seen = T.sync[0];
+        if (seen == 0) return;  // nothing stopped since the last rebuild
+        relist_running<NT>(T);
+        if (threadIdx.x == 0) atomicSub(&T.sync[0], seen);
+        return;
+    }
+    if (T.state[b] != 0) return;  // block-uniform
+    const size_t rstride = (size_t)T.B * T.d2p / 4;  // one row block, in f4v
+    float err = 0.f;
+    for (int j0 = 4 * threadIdx.x; j0 < T.d2; j0 += 4 * NT) {
+        const f4v *col = reinterpret_cast<const f4v *>(T.part + pidx(T, 0, 0, b, j0));
+        f4v cs = {0.f, 0.f, 0.f, 0.f};
+        for (int r0 = 0; r0 < T.R; r0 += 16) {
+            f4v v[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                v[q] = r0 + q < T.R ? col[(size_t)(r0 + q) * rstride] : f4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 16; ++q) cs += v[q];
+        }
+        const f4v bold = *reinterpret_cast<const f4v *>(T.bbuf + (size_t)(k & 1) * T.B * T.d2p + (size_t)b * T.d2p + j0);
+        f4v bnew;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int j = j0 + c;
+            float v = 0.f;  // padding columns
+            if (j < T.d2) {
+                const float nuj = T.nu[(size_t)b * T.d2 + j];
+                err += fabsf(cs[c] - nuj);
+                v = neg_inf();
+                if (nuj > 0.f) {
+                    if (cs[c] >= kSumLo && cs[c] <= kSumHi)
+                        v = bold[c] + log2f(nuj) - lg2(cs[c]);
+                    else
+                        v = log2f(nuj) - col_lse_exact(T, b, j);
+                }
+            }
+            bnew[c] = v;
+        }
+        *reinterpret_cast<f4v *>(T.bbuf + (size_t)((k + 1) & 1) * T.B * T.d2p + (size_t)b * T.d2p + j0) = bnew;
+    }
+    if (!(T.tol > 0.f)) return;
+    const float *re = T.rowerr + (size_t)(k & 1) * T.R * T.B;
+    for (int q = threadIdx.x; q < T.R; q += NT) err += re[(size_t)q * T.B + b];
+    err = block_sum_n<NT>(err, red);
+    if (threadIdx.x == 0 && err <= T.tol) {
+        T.state[b] = k;
+        if (T.order) atomicAdd(&T.sync[0], 1);
     }
 }
 
@@ -296,17 +371,6 @@ __device__ __forceinline__ void row_step(const Cost &cost, float ai, float mui, 
     if (lane == 0) *a_row = an;
 }
 
-// Early-stop test of problem b before sweep k (k >= 2): the marginal error of
-// iterate k-1 from the row-block and column-chunk partials, fixed order.
-__device__ __forceinline__ bool stop_before(const TiledArgs &T, int b, int k) {
-    if (!(T.tol > 0.f) || k < 2) return false;
-    const float *re = T.rowerr + (size_t)((k - 1) & 1) * T.R * T.B;
-    float err = 0.f;
-    for (int q = 0; q < T.R; ++q) err += re[(size_t)q * T.B + b];
-    for (int c = 0; c < T.JC; ++c) err += T.colerr[(size_t)b * T.JC + c];
-    return err <= T.tol;
-}
-
 // Sweep, one problem per work-group (per-sample costs, or tiny batches).
 // Work-group (row block r, problem b); wavefront w takes rows i0 + w,
 // i0 + w + 4, ...; lane l owns columns j = l + 64 c, c < NCW.  The
@@ -320,13 +384,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
     const int d1 = T.d1, d2 = T.d2;
 
     const int st = T.state[b];
-    if (!STATS) {
-        if (st != 0) return;
-        if (stop_before(T, b, k)) {
-            if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
-            return;
-        }
-    }
+    if (!STATS && st != 0) return;  // stopped by an earlier merge's test
     const int K = STATS ? (st ? st : T.n_iter) : k;
     const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
     const float *Cb = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0);
@@ -482,9 +540,8 @@ struct PointsShape {
 // exists).  Work-group (row block r, problem b) as in sk_tiled_sweep; lane l
 // keeps the centred, scaled coordinates of its columns j = l + 64 c in
 // registers.  The row's coordinates, potential and mass are loaded one row
-// ahead through a lane-varying index, so they arrive in vector registers
-// (vector operands taken from scalar registers issue at half rate on this
-// chip).
+// ahead (vector loads through a lane-varying index, kept in flight over the
+// current row's work).
 template <int NCW, int D, bool STATS>
 __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, int k) {
     extern __shared__ float lds[];  // [kWaves][NCW*64] column partials
@@ -494,13 +551,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, i
     const int d1 = T.d1, d2 = T.d2;
 
     const int st = T.state[b];
-    if (!STATS) {
-        if (st != 0) return;
-        if (stop_before(T, b, k)) {
-            if (r == 0 && threadIdx.x == 0) T.state[b] = k - 1;
-            return;
-        }
-    }
+    if (!STATS && st != 0) return;  // stopped by an earlier merge's test
     const int K = STATS ? (st ? st : T.n_iter) : k;
     const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
     float *ab = T.a + (size_t)b * d1;
@@ -598,51 +649,6 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep_points(TiledArgs T, i
     }
 }
 
-// Early-stop decision and compaction before sweep k (k >= 2, tol > 0) of the
-// shared-cost sweep: every running problem whose iterate k-1 met tol is
-// stopped (the same fixed-order test the sweeps otherwise take), and the
-// running ones are listed in increasing order, so that the sweep's
-// work-groups take only running problems (W per group) and whole groups of
-// stopped problems are never scheduled.  One work-group; a block-wide
-// prefix sum per 1024 problems keeps the order deterministic.
-constexpr int kCompactThreads = 1024;
-__global__ __launch_bounds__(kCompactThreads) void sk_tiled_compact(TiledArgs T, int k) {
-    __shared__ int wsum[kCompactThreads / 64];
-    __shared__ int base;
-    if (threadIdx.x == 0) base = 0;
-    __syncthreads();
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int b0 = 0; b0 < T.B; b0 += kCompactThreads) {
-        const int b = b0 + threadIdx.x;
-        bool live = false;
-        if (b < T.B && T.state[b] == 0) {
-            if (stop_before(T, b, k))
-                T.state[b] = k - 1;
-            else
-                live = true;
-        }
-        // exclusive prefix sum of the live flags: within the wavefront by
-        // ballot, across wavefronts through LDS
-        const unsigned long long m = __ballot(live);
-        const int before = __popcll(m & ((1ull << lane) - 1ull));
-        if (lane == 0) wsum[w] = __popcll(m);
-        __syncthreads();
-        int off = base;
-        for (int q = 0; q < w; ++q) off += wsum[q];
-        if (live) T.order[off + before] = b;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            int tot = 0;
-            for (int q = 0; q < kCompactThreads / 64; ++q) tot += wsum[q];
-            base += tot;
-        }
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) *T.nlive = base;
-}
-
-typedef float f4v __attribute__((ext_vector_type(4)));
-
 // Sweep for a cost shared by the batch (Section 4's setting).
 //
 // A work-group of W wavefronts = W problems of group g walks the rows of row
@@ -728,24 +734,16 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int d1 = T.d1, d2 = T.d2;
     // Problem of this wavefront: slot g W + w of the running list when the
-    // batch is compacted (the stop test already taken), else problem g W + w.
-    const bool compacted = !STATS && T.order && k >= 2;
+    // batch is compacted, else problem g W + w.
+    const bool compacted = !STATS && T.order;
     const int slot = g * W + w;
     const int nslot = compacted ? __builtin_amdgcn_readfirstlane(*T.nlive) : T.B;
     const int b_raw = slot < nslot ? (compacted ? __builtin_amdgcn_readfirstlane(T.order[slot]) : slot) : T.B;
     // Inactive wavefronts (past the batch, or stopped) keep staging and
     // reaching the barriers; they compute nothing and store nothing.
     const int b = b_raw < T.B ? b_raw : T.B - 1;
-    bool skip = b_raw >= T.B;
     const int st = T.state[b];
-    if (!STATS && !skip && !compacted) {
-        if (st != 0) {
-            skip = true;
-        } else if (stop_before(T, b, k)) {
-            if (r == 0 && lane == 0) T.state[b] = k - 1;
-            skip = true;
-        }
-    }
+    const bool skip = b_raw >= T.B || (!STATS && st != 0);
     if (!__syncthreads_or(!skip)) return;
 
     // Columns past d2 hold the padding cost (plan entries exactly 0); loads
@@ -1338,7 +1336,7 @@ void row_blocks(int B, int d1, int d2, int kind, int *R, int *RBS) {
 }
 
 struct Layout {
-    size_t bbuf, part, rowerr, lossp, colerr, state, order, a2, ctr, total;
+    size_t bbuf, part, rowerr, lossp, state, order, a2, ctr, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1378,10 +1376,8 @@ Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC
     off = align256(off + sizeof(float) * 3 * (size_t)R * B);
     L.lossp = off;
     off = align256(off + sizeof(float) * (size_t)R * B);
-    L.colerr = off;
-    off = align256(off + sizeof(float) * (size_t)B * JC);
-    L.state = off;
-    off = align256(off + sizeof(int32_t) * (size_t)B);
+    L.state = off;  // state[B], sync[4]
+    off = align256(off + sizeof(int32_t) * ((size_t)B + 4));
     L.order = off;  // order[B] then nlive
     if (kind == kKindShared) off = align256(off + sizeof(int32_t) * ((size_t)B + 1));
     L.a2 = off;
@@ -1395,6 +1391,14 @@ Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC
     return L;
 }
 
+// Raise a kernel's dynamic LDS limit when it needs more than the default 64 KB.
+template <class Kernel>
+hipError_t allow_lds(Kernel *kernel, size_t bytes) {
+    if (bytes <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)bytes);
+}
+
 // Launch sequence: init, exact first v-update (+ merge), n sweeps with a merge
 // after each but the last, stats sweep, final.
 template <class Sweep, class Stats>
@@ -1404,10 +1408,16 @@ hipError_t run_sequence(const TiledArgs &T, hipStream_t st, Sweep sweep, Stats s
     if (T.n_iter > 0) {
         hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
         const dim3 mblk(kMergeThreads);
-        hipLaunchKernelGGL(sk_tiled_merge<true>, dim3(T.JC, T.B), mblk, 0, st, T, 0);
+        hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), mblk, 0, st, T);
         for (int k = 1; k <= T.n_iter; ++k) {
             sweep(k);
-            if (k < T.n_iter) hipLaunchKernelGGL(sk_tiled_merge<false>, dim3(T.JC, T.B), mblk, 0, st, T, k);
+            if (k < T.n_iter) {
+                const dim3 mg(T.B + (T.order ? 1 : 0));
+                if (T.d2 > 1024)
+                    hipLaunchKernelGGL(sk_tiled_merge_cols<1024>, mg, dim3(1024), 0, st, T, k);
+                else
+                    hipLaunchKernelGGL(sk_tiled_merge_cols<256>, mg, dim3(256), 0, st, T, k);
+            }
         }
     }
     stats();
@@ -1429,19 +1439,16 @@ template <int NC4>
 hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
     constexpr int W = StreamShape<NC4>::W, NB = StreamShape<NC4>::NB;
     const size_t lds = sizeof(float) * W * NB * 256 * NC4;
-    static bool attr = false;  // rings above 64 KB need the larger dynamic LDS limit
-    if (!attr) {
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_stream<NC4, false>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_stream<NC4, true>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        attr = true;
-    }
+    // Rings above 64 KB need the larger dynamic LDS limit (set on every call:
+    // the library keeps no state of its own).
+    hipError_t e = allow_lds(&sk_tiled_sweep_stream<NC4, false>, lds);
+    if (e == hipSuccess) e = allow_lds(&sk_tiled_sweep_stream<NC4, true>, lds);
+    if (e != hipSuccess) return e;
     const dim3 grid(T.R, T.B), blk(64 * W);
     hipLaunchKernelGGL(sk_tiled_init, dim3(512), dim3(kThreads), 0, st, T);
     if (T.n_iter > 0) {
         hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
-        hipLaunchKernelGGL(sk_tiled_merge<true>, dim3(T.JC, T.B), dim3(kMergeThreads), 0, st, T, 0);
+        hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), dim3(kMergeThreads), 0, st, T);
         for (int k = 1; k <= T.n_iter; ++k)
             hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, false>), grid, blk, lds, st, T, k);
     }
@@ -1463,21 +1470,15 @@ template <int NCW, int W, bool VEC4>
 hipError_t run_shared(const TiledArgs &T, hipStream_t st) {
     constexpr int RS = SharedShape<NCW>::RS, RB = SharedShape<NCW>::RB;
     const size_t lds = sizeof(float) * 2 * RS * NCW * 64;
-    static bool attr = false;  // chunk buffers above 64 KB need the larger dynamic LDS limit
-    if (!attr) {
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        attr = true;
-    }
+    // Chunk buffers above 64 KB need the larger dynamic LDS limit (set on
+    // every call: the library keeps no state of its own).
+    hipError_t e = allow_lds(&sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>, lds);
+    if (e == hipSuccess) e = allow_lds(&sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>, lds);
+    if (e != hipSuccess) return e;
     const dim3 grid(T.R, (T.B + W - 1) / W), blk(64 * W);
     return run_sequence(
         T, st,
-        [&](int k) {
-            if (T.order && k >= 2) hipLaunchKernelGGL(sk_tiled_compact, dim3(1), dim3(kCompactThreads), 0, st, T, k);
-            hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>), grid, blk, lds, st, T, k);
-        },
+        [&](int k) { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, false>), grid, blk, lds, st, T, k); },
         [&]() { hipLaunchKernelGGL((sk_tiled_sweep_shared<NCW, W, RS, RB, VEC4, true>), grid, blk, lds, st, T, 0); });
 }
 
@@ -1564,8 +1565,8 @@ TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     T.part = reinterpret_cast<float *>(base + L.part);
     T.rowerr = reinterpret_cast<float *>(base + L.rowerr);
     T.lossp = reinterpret_cast<float *>(base + L.lossp);
-    T.colerr = reinterpret_cast<float *>(base + L.colerr);
     T.state = reinterpret_cast<int32_t *>(base + L.state);
+    T.sync = T.state + a.B;
     T.order = nullptr;
     T.nlive = nullptr;
     T.alpha_out = a.alpha;
@@ -1615,9 +1616,8 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     // 16-byte global->LDS copies need 16-byte aligned cost rows.
     const bool vec4 = a.d2 % 4 == 0 && ((uintptr_t)a.C % 16) == 0;
     // Early stop with W problems per work-group: compact the running
-    // problems before each sweep (diagnostic switch SK_TILED_COMPACT=0 off).
-    const char *cenv = getenv("SK_TILED_COMPACT");
-    if (W && a.tol > 0.f && !(cenv && !strcmp(cenv, "0"))) {
+    // problems before each sweep (unless sinkhorn_forward_select says not to).
+    if (W && a.tol > 0.f && a.select != SK_SELECT_NO_COMPACTION) {
         T.order = reinterpret_cast<int32_t *>(base + L.order);
         T.nlive = T.order + a.B;
     }

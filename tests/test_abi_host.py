@@ -37,8 +37,31 @@ def test_library_exports_every_declared_symbol():
     assert not [s for s in exported if s.startswith("_ZN2sk")]
 
 
+def test_library_reads_no_environment():
+    """No environment variable changes what the library computes: it imports
+    no getenv (kernel choices for tests go through sinkhorn_forward_select)."""
+    out = subprocess.run(["nm", "-D", "--undefined-only", sk.library_path()], capture_output=True, text=True,
+                         check=True).stdout
+    imported = {l.split()[-1].split("@")[0] for l in out.splitlines() if l.strip()}
+    assert not imported & {"getenv", "secure_getenv", "__secure_getenv"}
+
+
+def test_forward_select_rejects_unknown_selector():
+    lib = sk.load_library()
+    p = _binding.problem(4, 10, 10, 0, 0.1, 10)
+    v = None
+    for sel in (-1, 5, 1 << 20):
+        assert lib.sinkhorn_forward_select(ctypes.byref(p), sel, v, v, v, v, v, v, v, v, v, 0, None) == -7
+    # a valid selector goes on to the ordinary checks
+    assert lib.sinkhorn_forward_select(ctypes.byref(p), 2, v, v, v, v, v, v, v, v, v, 0, None) == -1
+    assert lib.sinkhorn_forward_select(ctypes.byref(_binding.problem(4, 10, 10, 0, 0.0, 10)), 1, v, v, v, v, v, v,
+                                       v, v, v, 0, None) == -3
+    with pytest.raises(ValueError):
+        sk.sinkhorn_forward_select("fast", None, None, None, 0.1, 10)
+
+
 def test_status_strings():
-    for code in range(-6, 1):
+    for code in range(-7, 1):
         assert sk.sinkhorn_status_string(code)
     assert "lambda" in sk.sinkhorn_status_string(-3)
     assert sk.sinkhorn_status_string(-99) == "unknown status"

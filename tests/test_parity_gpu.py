@@ -22,10 +22,26 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# Kernel selector of the forwards run by _gpu (sinkhorn_forward_select):
+# "default" is sinkhorn_forward itself; tests pin other kernels with set_form.
+_FORM = {"select": "default"}
+
+
+def set_form(select):
+    _FORM["select"] = "default" if select == "auto" else select
+
+
+@pytest.fixture(autouse=True)
+def _default_form():
+    set_form("default")
+    yield
+    set_form("default")
+
+
 def _gpu(prob, sample=None):
     mu, nu, C = prob.mu, prob.nu, prob.C
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
-    out = sk.sinkhorn_forward(t(mu), t(nu), t(C), prob.lam, prob.n_iter, prob.tol)
+    out = sk.sinkhorn_forward_select(_FORM["select"], t(mu), t(nu), t(C), prob.lam, prob.n_iter, prob.tol)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}
 
@@ -93,11 +109,11 @@ def check_backward(prob, gpu, ref, idx=None, grad_C=False, seed=0):
 
 
 @pytest.fixture(params=["auto", "nosym", "log"])
-def form(request, monkeypatch):
+def form(request):
     """Resident regime: the plain-form kernels with their fallbacks (the
     default), the same without the symmetric-cost kernel (symmetric costs go
     to the general kernel), or the log-domain kernel alone."""
-    monkeypatch.setenv("SK_RESIDENT_FORM", request.param)
+    set_form(request.param)
     return request.param
 
 
@@ -226,11 +242,11 @@ def test_autograd_wrapper(form):
 
 # ---------------------------------------------------------------- plain form and its fallback
 
-def test_plain_form_takes_in_range_problems(monkeypatch):
+def test_plain_form_takes_in_range_problems():
     """The plain-form kernel alone (no fallback launch) solves every label
     problem (cost spread 54 bits) and leaves a lambda = 1e-3 grid problem
     (spread > 1000 bits) to the log-domain kernel: iters = -1."""
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     prob = workloads.make_config(2, B=32)
     gpu, ref = check_forward(prob)
     assert np.all(gpu["iters"] == prob.n_iter)
@@ -239,17 +255,17 @@ def test_plain_form_takes_in_range_problems(monkeypatch):
     assert np.all(_gpu(far)["iters"] == -1)
 
 
-def test_plain_fallback_mixed_batch(monkeypatch):
+def test_plain_fallback_mixed_batch():
     """Per-sample costs where every third problem's cost spread exceeds the
     plain form's range: with the fallback every problem matches the oracle;
     without it exactly those problems come back unsolved."""
     prob = workloads.random_problem(seed=17, B=9, d1=50, d2=60, lam=0.05, n_iter=80, c_batched=True)
     far = np.arange(prob.B) % 3 == 0
     prob.C[far] *= 3.0  # spread 3 * 28.9 bits > 64
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     alone = _gpu(prob)
     assert np.all((alone["iters"] == -1) == far)
-    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    set_form("auto")
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
     near = ~far
@@ -257,11 +273,11 @@ def test_plain_fallback_mixed_batch(monkeypatch):
         np.testing.assert_array_equal(gpu[k][near], alone[k][near])
 
 
-def test_plain_early_stop_agrees_with_log(monkeypatch):
+def test_plain_early_stop_agrees_with_log():
     prob = workloads.random_problem(seed=18, B=8, d1=64, d2=48, lam=0.1, n_iter=300, tol=1e-5)
     out = {}
     for f in ("plain", "log"):
-        monkeypatch.setenv("SK_RESIDENT_FORM", f)
+        set_form(f)
         out[f] = check_forward(prob)[0]
     assert np.all(out["plain"]["iters"] >= 0)
     assert np.all(np.abs(out["plain"]["iters"] - out["log"]["iters"]) <= 1)
@@ -270,50 +286,50 @@ def test_plain_early_stop_agrees_with_log(monkeypatch):
 # ---------------------------------------------------------------- symmetric shared cost, one wavefront per problem
 
 @pytest.mark.parametrize("d", [1, 2, 7, 8, 9, 16, 17, 32, 33, 64, 65, 96, 97, 100, 104])
-def test_sym_kernel_shapes(d, monkeypatch):
+def test_sym_kernel_shapes(d):
     """Every register-tile width of the symmetric-cost kernel, ragged tails
     included; alone (plain) it solves every problem."""
     prob = workloads.random_problem(seed=300 + d, B=5, d1=d, d2=d, lam=0.1, n_iter=60, cost="sym")
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_sym_kernel_zero_masses(monkeypatch):
+def test_sym_kernel_zero_masses():
     prob = workloads.random_problem(seed=31, B=7, d1=90, d2=90, lam=0.05, n_iter=120, cost="sym", zero_frac=0.3)
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_sym_kernel_runs_general_iteration_on_asymmetric_cost(monkeypatch):
+def test_sym_kernel_runs_general_iteration_on_asymmetric_cost():
     """An asymmetric cost (one pair differs): the symmetric kernel alone runs
     the general iteration in place, with the same bits as the general kernel
     launched by itself, and the result matches the oracle."""
     prob = workloads.random_problem(seed=32, B=6, d1=50, d2=50, lam=0.1, n_iter=50, cost="sym")
     prob.C[0, 3, 41] += 0.25
-    monkeypatch.setenv("SK_RESIDENT_FORM", "nosym")
+    set_form("nosym")
     ref_bits = _gpu(prob)
     assert np.all(ref_bits["iters"] == 50)
     for form in ("plain", "auto"):
-        monkeypatch.setenv("SK_RESIDENT_FORM", form)
+        set_form(form)
         gpu, ref = check_forward(prob)
         for k in ("alpha", "beta", "loss", "marg_err", "iters"):
             np.testing.assert_array_equal(gpu[k], ref_bits[k])
 
 
-def test_sym_kernel_hands_over_out_of_range(monkeypatch):
+def test_sym_kernel_hands_over_out_of_range():
     """lambda = 1e-3 on a symmetric 1-D grid cost (spread > 1000 bits): iters
     = -1 from the symmetric kernel alone; the log-domain kernel solves it."""
     prob = workloads.random_problem(seed=33, B=3, d1=60, d2=60, lam=1e-3, n_iter=100, cost="grid1d")
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     assert np.all(_gpu(prob)["iters"] == -1)
-    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    set_form("auto")
     check_forward(prob, merr_atol=1e-4)
 
 
 @pytest.mark.parametrize("tol,n_iter", [(0.0, 50), (1e-5, 300)])
-def test_sym_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
+def test_sym_kernel_guard_fails_in_loop(tol, n_iter):
     """A positive but tiny mass (1e-37) puts its row scaling below 2^-100 in
     the first u-update, a guard the symmetric kernel checks inside the
     iteration (the cost spread itself is in range): alone it returns that
@@ -321,12 +337,12 @@ def test_sym_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
     problem matches the oracle and the others keep their bits."""
     prob = workloads.random_problem(seed=35, B=6, d1=70, d2=70, lam=0.1, n_iter=n_iter, cost="sym", tol=tol)
     prob.mu[2, 5] = 1e-37
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     alone = _gpu(prob)
     rest = np.arange(prob.B) != 2
     assert alone["iters"][2] == -1
     assert np.all(alone["iters"][rest] >= 1)
-    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    set_form("auto")
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref)
     for k in ("alpha", "beta", "loss", "marg_err", "iters"):
@@ -334,19 +350,19 @@ def test_sym_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
 
 
 @pytest.mark.parametrize("tol,n_iter", [(0.0, 50), (1e-5, 300)])
-def test_gen_kernel_guard_fails_in_loop(tol, n_iter, monkeypatch):
+def test_gen_kernel_guard_fails_in_loop(tol, n_iter):
     """Per-sample costs, d1 != d2: a tiny positive mass (1e-37) fails a guard
     of the general kernel inside the iteration; alone it returns that
     problem unsolved and the rest solved, with the fallback the problem
     matches the oracle and the others keep their bits."""
     prob = workloads.random_problem(seed=38, B=5, d1=60, d2=45, lam=0.1, n_iter=n_iter, c_batched=True, tol=tol)
     prob.mu[1, 9] = 1e-37
-    monkeypatch.setenv("SK_RESIDENT_FORM", "plain")
+    set_form("plain")
     alone = _gpu(prob)
     rest = np.arange(prob.B) != 1
     assert alone["iters"][1] == -1
     assert np.all(alone["iters"][rest] >= 1)
-    monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+    set_form("auto")
     gpu, ref = check_forward(prob)
     check_backward(prob, gpu, ref, grad_C=True)
     for k in ("alpha", "beta", "loss", "marg_err", "iters"):
@@ -370,11 +386,11 @@ def test_gen_kernel_full_batch_per_sample_sampled():
     check_backward(prob, gpu, ref, idx=idx, grad_C=True)
 
 
-def test_sym_kernel_early_stop(monkeypatch):
+def test_sym_kernel_early_stop():
     prob = workloads.random_problem(seed=34, B=8, d1=80, d2=80, lam=0.1, n_iter=400, tol=1e-5, cost="sym")
     out = {}
     for f in ("plain", "log"):
-        monkeypatch.setenv("SK_RESIDENT_FORM", f)
+        set_form(f)
         out[f] = check_forward(prob)[0]
     assert np.all(out["plain"]["iters"] >= 1) and np.all(out["plain"]["iters"] < 400)
     assert np.all(np.abs(out["plain"]["iters"] - out["log"]["iters"]) <= 1)
@@ -562,16 +578,16 @@ def test_stream_small_lambda_exact_paths():
 
 # ---------------------------------------------------------------- early stop with batch compaction (shared sweep)
 
-def test_shared_sweep_early_stop_compaction(monkeypatch):
+def test_shared_sweep_early_stop_compaction():
     """Image histograms with an early stop: problems stop at different
     iterations; the shared-cost sweep compacts the running problems into its
     8-problem work-groups.  Parity with the oracle at the GPU's iteration
     counts, and the same bits as without compaction."""
     prob = workloads.make_config(3, B=24, side=20, n_iter=400)
     prob.tol = 2e-4
-    monkeypatch.setenv("SK_TILED_COMPACT", "0")
+    set_form("nocompact")
     plain = _gpu(prob)
-    monkeypatch.delenv("SK_TILED_COMPACT")
+    set_form("default")
     gpu, ref = check_forward(prob)
     its = gpu["iters"]
     assert (its < prob.n_iter).sum() >= prob.B - 2 and len(set(its.tolist())) > 3, its
@@ -581,7 +597,7 @@ def test_shared_sweep_early_stop_compaction(monkeypatch):
 
 # ---------------------------------------------------------------- randomized resident problems
 
-def test_random_resident_problems(monkeypatch):
+def test_random_resident_problems():
     """Forty seeded random problems of the resident regime (d1, d2 <= 128,
     shared or per-sample, symmetric or not, zero masses, lambda over two
     decades so that some leave the plain form's range, fixed or early-stopped
@@ -599,7 +615,7 @@ def test_random_resident_problems(monkeypatch):
         cb = bool(rng.random() < 0.4)
         zf = float(rng.choice([0.0, 0.0, 0.2]))
         cost = "sym" if (d1 == d2 and rng.random() < 0.6) else "uniform"
-        monkeypatch.setenv("SK_RESIDENT_FORM", "nosym" if rng.random() < 0.25 else "auto")
+        set_form("nosym" if rng.random() < 0.25 else "auto")
         prob = workloads.random_problem(seed=int(rng.integers(1 << 30)), B=B, d1=d1, d2=d2, lam=lam,
                                         n_iter=n_iter, c_batched=cb, zero_frac=zf, cost=cost, tol=tol)
         _say(f"[random {case}]")
@@ -607,7 +623,7 @@ def test_random_resident_problems(monkeypatch):
         check_backward(prob, gpu, ref, grad_C=True)
 
 
-def test_random_asymmetric_shared_costs(monkeypatch):
+def test_random_asymmetric_shared_costs():
     """Twelve seeded shared square costs, symmetric but for one pair, over the
     symmetric kernel's size buckets (d up to 104): each work-group finds the
     pair and runs the general iteration in place.  Same bits as the general
@@ -624,9 +640,9 @@ def test_random_asymmetric_shared_costs(monkeypatch):
         j = (i + 1 + int(rng.integers(0, d - 1))) % d  # j != i
         prob.C[0, i, j] += 0.01
         _say(f"[asym {case}] d={d} pair=({i},{j})")
-        monkeypatch.setenv("SK_RESIDENT_FORM", "nosym")
+        set_form("nosym")
         ref_bits = _gpu(prob)
-        monkeypatch.setenv("SK_RESIDENT_FORM", "auto")
+        set_form("auto")
         gpu, ref = check_forward(prob)
         for k in ("alpha", "beta", "loss", "marg_err", "iters"):
             np.testing.assert_array_equal(gpu[k], ref_bits[k])
@@ -634,11 +650,11 @@ def test_random_asymmetric_shared_costs(monkeypatch):
 
 
 @pytest.mark.parametrize("form,c_batched", [("auto", False), ("nosym", False), ("log", False), ("auto", True)])
-def test_large_batch_resident(form, c_batched, monkeypatch):
+def test_large_batch_resident(form, c_batched):
     """B = 70000 small problems (more than 65535 work-groups for the plain
     kernels, problem indices past 16 bits) through each resident kernel; the
     oracle checks samples on both sides of 65536."""
-    monkeypatch.setenv("SK_RESIDENT_FORM", form)
+    set_form(form)
     prob = workloads.random_problem(seed=77, B=70000, d1=8, d2=8, lam=0.1, n_iter=50, c_batched=c_batched,
                                     cost="uniform" if c_batched else "sym")
     gpu = _gpu(prob)
@@ -646,6 +662,35 @@ def test_large_batch_resident(form, c_batched, monkeypatch):
     idx = np.array([0, 1, 32767, 65535, 65536, 65537, 69998, 69999])
     gpu, ref = check_forward(prob, gpu=gpu, idx=idx)
     check_backward(prob, gpu, ref, idx=idx, grad_C=c_batched)
+
+
+def test_tiled_on_side_stream():
+    """The tiled regime on a caller's side stream while the current stream
+    allocates and fills memory: the binding allocates the outputs and the
+    temporary workspace on the library's stream, so the caching allocator
+    never hands the freed workspace to other work before the kernels end."""
+    prob = workloads.make_config(3, B=16, n_iter=60)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    mu, nu, C = t(prob.mu), t(prob.nu), t(prob.C)
+    need = sk.sinkhorn_workspace_bytes(prob.B, prob.d1, prob.d2, 0, prob.lam, prob.n_iter)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    out = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter, stream=side)
+    junk = [torch.full((need // 4 + 1,), float("nan"), device=DEV) for _ in range(8)]
+    side.synchronize()
+    torch.cuda.synchronize()
+    del junk
+    gpu = {k: v.cpu().numpy() for k, v in out.items()}
+    check_forward(prob, gpu=gpu)
+
+
+def test_shared_grad_C_many_rows():
+    """A shared cost with d1 = 70000 rows (more than a grid's y dimension):
+    the forward runs in the tiled regime and grad_C (rows grid-strided) covers
+    every row; the oracle checks the whole gradient."""
+    prob = workloads.random_problem(seed=79, B=2, d1=70000, d2=130, lam=0.2, n_iter=8)
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
 
 
 def test_tiled_max_batch():
