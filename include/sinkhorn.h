@@ -149,6 +149,32 @@ SK_API sk_status sinkhorn_forward_select(const sk_problem *p, int32_t select, co
                                          size_t ws_bytes, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the forward
+ * of sinkhorn_forward without a workspace argument.  Its scratch is a fixed
+ * device array of SINKHORN_NOALLOC_SCRATCH_BYTES inside the library, one per
+ * GPU, allocated when the library's code object is loaded and held until the
+ * process ends; the call itself allocates and frees nothing.  The caller
+ * still owns every input and output.  It runs on the current device (the
+ * stream must belong to it).
+ *   - Problems whose sinkhorn_workspace_bytes(p) exceeds the array are
+ *     rejected with SK_ERR_WORKSPACE before anything is launched (problems
+ *     that need no workspace always fit).
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents (the kernels initialise what they read).  Calls that
+ *     overlap on one GPU, on any streams or threads, race and give
+ *     unspecified results: serialise them.
+ *   - The first call on a device looks up the array's device address
+ *     (SK_ERR_HIP if that fails).
+ * Results are those of sinkhorn_forward on the same inputs.
+ */
+#define SINKHORN_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+SK_API sk_status sinkhorn_forward_noalloc(const sk_problem *p, const float *mu, const float *nu,
+                                          const float *C, float *alpha, float *beta, float *loss,
+                                          float *marg_err, int32_t *iters, void *stream);
+
+/*
  * Backward (Section 2): the Lagrange-multiplier gradient of the entropic
  * objective W_lambda(mu, nu) = min_U E^lambda, taken at the iterate the
  * forward returned (Section 5 explains why this is used for the E^0 loss).

@@ -10,6 +10,7 @@ passes raw device pointers and the current HIP stream.  There is no CPU
 fallback -- without the built library every call raises.
 """
 from ._binding import (  # noqa: F401
+    NOALLOC_SCRATCH_BYTES,
     SinkhornError,
     library_path,
     load_library,
@@ -17,6 +18,7 @@ from ._binding import (  # noqa: F401
     sinkhorn_backward_points,
     sinkhorn_backward_sharp,
     sinkhorn_forward,
+    sinkhorn_forward_noalloc,
     sinkhorn_forward_points,
     sinkhorn_forward_select,
     sinkhorn_points_workspace_bytes,
@@ -27,6 +29,7 @@ from ._binding import (  # noqa: F401
 from .loss import SinkhornLoss, SinkhornPointsLoss, sinkhorn_loss, sinkhorn_loss_points  # noqa: F401
 
 __all__ = [
+    "NOALLOC_SCRATCH_BYTES",
     "SinkhornError",
     "SinkhornLoss",
     "SinkhornPointsLoss",
@@ -36,6 +39,7 @@ __all__ = [
     "sinkhorn_backward_points",
     "sinkhorn_backward_sharp",
     "sinkhorn_forward",
+    "sinkhorn_forward_noalloc",
     "sinkhorn_forward_points",
     "sinkhorn_forward_select",
     "sinkhorn_loss",

@@ -29,6 +29,7 @@ EXPORTED = (
     "sinkhorn_workspace_bytes",
     "sinkhorn_forward",
     "sinkhorn_forward_select",
+    "sinkhorn_forward_noalloc",
     "sinkhorn_backward",
     "sinkhorn_status_string",
     "sinkhorn_regime",
@@ -79,6 +80,8 @@ def load_library():
     lib.sinkhorn_forward.restype = ctypes.c_int
     lib.sinkhorn_forward_select.argtypes = [PP, ctypes.c_int32, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     lib.sinkhorn_forward_select.restype = ctypes.c_int
+    lib.sinkhorn_forward_noalloc.argtypes = [PP, P, P, P, P, P, P, P, P, P]
+    lib.sinkhorn_forward_noalloc.restype = ctypes.c_int
     lib.sinkhorn_backward.argtypes = [PP, P, P, P, P, P, P, P, P, P, P]
     lib.sinkhorn_backward.restype = ctypes.c_int
     lib.sinkhorn_status_string.argtypes = [ctypes.c_int]
@@ -187,6 +190,32 @@ def sinkhorn_forward(mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=Non
     Returns dict(alpha [B,d1], beta [B,d2], loss [B], marg_err [B], iters [B] int32).
     """
     return _forward(0, mu, nu, C, lam, n_iter, tol, stream, workspace)
+
+
+# Size of the library's fixed scratch array (SINKHORN_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def sinkhorn_forward_noalloc(mu, nu, C, lam, n_iter, tol=0.0, stream=None, out=None):
+    """Forward through the entry point that allocates nothing: its scratch is
+    the library's fixed per-GPU array.  out (optional) = dict of preallocated
+    outputs (alpha, beta, loss, marg_err, iters), else they are allocated here."""
+    lib = load_library()
+    _dev(mu, "mu"), _dev(nu, "nu"), _dev(C, "C")
+    B, d1, d2, cb = _shapes(mu, nu, C)
+    p = problem(B, d1, d2, cb, lam, n_iter, tol)
+    dev = mu.device
+    if out is None:
+        f = dict(device=dev, dtype=torch.float32)
+        with _on(stream):
+            out = dict(alpha=torch.empty((B, d1), **f), beta=torch.empty((B, d2), **f), loss=torch.empty((B,), **f),
+                       marg_err=torch.empty((B,), **f), iters=torch.empty((B,), device=dev, dtype=torch.int32))
+    st = lib.sinkhorn_forward_noalloc(ctypes.byref(p), _ptr(mu), _ptr(nu), _ptr(C), _ptr(out["alpha"]),
+                                      _ptr(out["beta"]), _ptr(out["loss"]), _ptr(out["marg_err"]),
+                                      _ptr(out["iters"]), _stream(dev, stream))
+    if st != 0:
+        raise SinkhornError(st, "sinkhorn_forward_noalloc")
+    return out
 
 
 def sinkhorn_forward_select(select, mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None):

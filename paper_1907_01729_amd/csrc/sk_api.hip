@@ -3,6 +3,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "sk_internal.h"
 
 namespace {
@@ -114,6 +116,31 @@ size_t cost_bytes(const sk_problem *p) {
     return (n + 255) & ~size_t(255);
 }
 
+// ---- fixed scratch of sinkhorn_forward_noalloc ----
+//
+// One array per GPU, allocated when the code object is loaded and held until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: its device address is taken once per device with
+// hipGetSymbolAddress and only that address is handed to kernels.
+__device__ __align__(256) unsigned char scratch[SINKHORN_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (null on failure).
+void *device_scratch() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -170,6 +197,21 @@ sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu
                            size_t ws_bytes, void *stream) {
     return sinkhorn_forward_select(p, SK_SELECT_DEFAULT, mu, nu, C, alpha, beta, loss, marg_err, iters, workspace,
                                    ws_bytes, stream);
+}
+
+sk_status sinkhorn_forward_noalloc(const sk_problem *p, const float *mu, const float *nu, const float *C,
+                                   float *alpha, float *beta, float *loss, float *marg_err, int32_t *iters,
+                                   void *stream) {
+    sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (p->B == 0) return SK_OK;
+    if (!mu || !nu || !C || !alpha || !beta || !loss || !marg_err || !iters) return SK_ERR_NULLPTR;
+    const size_t need = sinkhorn_workspace_bytes(p);
+    if (need > SINKHORN_NOALLOC_SCRATCH_BYTES) return SK_ERR_WORKSPACE;
+    void *ws = nullptr;
+    if (need > 0 && !(ws = device_scratch())) return SK_ERR_HIP;
+    const sk::FwdArgs a = fwd_args(p, mu, nu, C, alpha, beta, loss, marg_err, iters);
+    return run_forward(a, ws, static_cast<hipStream_t>(stream)) == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 
 sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu,
