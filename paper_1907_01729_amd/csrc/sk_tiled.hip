@@ -827,35 +827,54 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
             if (!skip) {
                 const int rr0 = rel & 63;
                 float ai[RB], e[RB][NCW], p[RB], f[RB];
-                // Every staged cost value of the batch goes into the plan-entry
-                // registers first (one LDS latency per batch), then each is
-                // turned into its plan entry in place.  Rows past the block
-                // (a = -inf) read the batch's first row, which is staged.
+                // The staged cost values of the batch go into the plan-entry
+                // registers and are turned into plan entries in place, in
+                // groups of G: group g + 1 is read from LDS while group g's
+                // exponentials run, so the LDS reads of every wavefront spread
+                // over its arithmetic instead of stalling it once per batch.
+                // Rows past the block (a = -inf) read the batch's first row,
+                // which is staged.
+                constexpr int NE = RB * NCW, G = RB > 1 ? NCW : 16, NG = (NE + G - 1) / G;
+                int rq[RB];
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
-                    const int rq = rel + q < nrows ? rb + q : rb;
-#pragma unroll
-                    for (int c = 0; c < NCW; ++c) e[q][c] = cbuf[rq * D2P + 64 * c];
+                    rq[q] = rel + q < nrows ? rb + q : rb;
+                    ai[q] = uni(a_seg, rr0 + q);
                 }
+                auto read_group = [&](int g) {
+#pragma unroll
+                    for (int n = g * G; n < (g + 1) * G && n < NE; ++n)
+                        e[n / NCW][n % NCW] = cbuf[rq[n / NCW] * D2P + 64 * (n % NCW)];
+                };
+                read_group(0);
                 __builtin_amdgcn_sched_barrier(0);
                 // The exponentials at the lowest issue priority, the batch's
                 // serial reduction and update at the highest, so that another
                 // wavefront's exponentials fill this one's reduction latency.
                 __builtin_amdgcn_s_setprio(0);
 #pragma unroll
-                for (int q = 0; q < RB; ++q) {
-                    ai[q] = uni(a_seg, rr0 + q);
+                for (int g = 0; g < NG; ++g) {
+                    if (g + 1 < NG) read_group(g + 1);
 #pragma unroll
-                    for (int c = 0; c < NCW; ++c) e[q][c] = ex2(__builtin_fmaf(e[q][c], ns, ai[q] + bv[c]));
-                    p[q] = tree_sum<NCW>(e[q]);
+                    for (int n = g * G; n < (g + 1) * G && n < NE; ++n) {
+                        const int q = n / NCW, c = n % NCW;
+                        e[q][c] = ex2(__builtin_fmaf(e[q][c], ns, ai[q] + bv[c]));
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
+#pragma unroll
+                for (int q = 0; q < RB; ++q) p[q] = tree_sum<NCW>(e[q]);
                 __builtin_amdgcn_s_setprio(3);
                 // Row updates of the batch, one row per 16-lane group (the
                 // all-reduce's packed layout): each lane fetches its row's
                 // potential and mass from the segment registers.
                 const float rsv = allreduce_rows_packed<RB>(p);
+                // Each lane's row of the packed layout: its potential and mass
+                // (one row per batch: wave-uniform, read with readlane instead
+                // of an LDS permute).
                 const int src = rr0 + row_of_lane<RB>(lane);
-                const float av = lane_get(a_seg, src), muv = lane_get(mu_seg, src);
+                const float av = RB == 1 ? ai[0] : lane_get(a_seg, src);
+                const float muv = RB == 1 ? uni(mu_seg, rr0) : lane_get(mu_seg, src);
                 bool exact_any = false;
                 if (STATS) {
                     rowerr += muv > 0.f ? fabsf(rsv - muv) : 0.f;
@@ -871,15 +890,16 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                 } else {
                     const bool inr = rsv >= kSumLo && rsv <= kSumHi;
                     const bool upd = muv > 0.f && inr;
-                    const float an = av + lane_get(lmu_seg, src) - lg2(rsv);
+                    const float an = av + (RB == 1 ? uni(lmu_seg, rr0) : lane_get(lmu_seg, src)) - lg2(rsv);
                     const float fv = upd ? ex2(an - av) : 0.f;
                     rowerr += upd ? fabsf(fv * rsv - muv) : 0.f;
                     exact_any = __any(muv > 0.f && !inr);
 #pragma unroll
-                    for (int q = 0; q < RB; ++q) f[q] = uni(fv, lane_of_row<RB>(q));
+                    for (int q = 0; q < RB; ++q) f[q] = RB == 1 ? fv : uni(fv, lane_of_row<RB>(q));
                     // lane rr0 + q takes row q's new potential
                     const int dq = lane - rr0;
-                    const float got = lane_get(upd ? an : av, lane_of_row<RB>(dq >= 0 && dq < RB ? dq : 0));
+                    const float got =
+                        RB == 1 ? (upd ? an : av) : lane_get(upd ? an : av, lane_of_row<RB>(dq >= 0 && dq < RB ? dq : 0));
                     a_out = dq >= 0 && dq < RB ? got : a_out;
                 }
                 __builtin_amdgcn_s_setprio(0);
@@ -1463,7 +1483,7 @@ hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
 template <int NCW>
 struct SharedShape {
     static constexpr int RB = NCW <= 16 ? 4 : (NCW <= 32 ? 2 : 1);
-    static constexpr int RS = NCW <= 16 ? 8 : (NCW <= 32 ? 4 : 2);
+    static constexpr int RS = NCW <= 16 ? 8 : 4;
 };
 
 template <int NCW, int W, bool VEC4>
