@@ -182,6 +182,9 @@ def main():
                     help="override the workload's iteration count (short runs under a profiler); the line names it")
     ap.add_argument("--tol", type=float, default=None,
                     help="override the workload's early-stop tolerance on the marginal L1 error")
+    ap.add_argument("--select", default="default", choices=["default", "log", "plain", "nosym", "nocompact"],
+                    help="forward through sinkhorn_forward_select with these kernels pinned (resident shapes: "
+                         "'log' times the log-domain kernel alone); the line names it")
     ap.add_argument("--sharp", action="store_true",
                     help="backward = gradient of E^0 itself (implicit differentiation, conjugate gradients; "
                          "resident shapes: configs 1 and 2)")
@@ -242,6 +245,8 @@ def main():
         ws = torch.empty((max(nws, 1),), device=dev, dtype=torch.uint8)
 
         def fwd(n):
+            if args.select != "default":
+                return sk.sinkhorn_forward_select(args.select, mu, nu, C, prob.lam, n, prob.tol, workspace=ws)
             return sk.sinkhorn_forward(mu, nu, C, prob.lam, n, prob.tol, workspace=ws)
 
         def bwd(out):
@@ -290,7 +295,26 @@ def main():
     bwd_ms = float(np.mean([a.elapsed_time(b) for a, b in bev]))
 
     # Roofline of the dominant kernel.
-    if regime == 1:
+    if regime == 1 and args.select == "log":
+        # The log-domain kernel alone: one launch per forward.  Algorithmic
+        # work: one exp2 per cell per iteration, plus the first (exact)
+        # v-update and the closing measurement: (iters + 2) d1 d2 per problem.
+        kname = "sk_resident_log_kernel"
+        kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for k in range(args.steps):
+            kev[k][0].record(stream)
+            fwd(prob.n_iter)
+            kev[k][1].record(stream)
+        torch.cuda.synchronize()
+        kernel_ms = float(np.mean([a.elapsed_time(b) for a, b in kev]))
+        exps = float(np.sum(iters + 2.0)) * prob.d1 * prob.d2
+        achieved = exps / (kernel_ms * 1e-3) / 1e12
+        src = kernel_source_hash(["sk_resident.hip", "sk_resident_log.h", "sk_resident_gen.h", "sk_device.h"])
+        roof = dict(bound="alu", achieved=round(achieved, 4), peak=round(PEAK_EXP_TS, 4), unit="Texp/s",
+                    frac=round(achieved / PEAK_EXP_TS, 4),
+                    traffic=stored_traffic(f"{kname}_{prob.name}_counters.md", src), kernel=kname,
+                    kernel_ms=round(kernel_ms, 5), work="exp2 per launch = (iters + 2)*d1*d2 per problem")
+    elif regime == 1:
         # Resident regime: the first-choice plain-form kernel solves every
         # problem (the fallbacks launched after it find nothing to do).  Its
         # duration alone is taken with events around launches of that kernel
@@ -388,6 +412,7 @@ def main():
             **({"D": prob.D, "cost": "from points"} if points else {}),
             **({"backward": "sharp: gradient of E^0 by implicit differentiation (conjugate gradients)"}
                if args.sharp else {}),
+            **({"select": args.select} if args.select != "default" else {}),
             **({"overrides": {k: v for k, v in (("B", args.batch or None), ("tol", args.tol),
                                                  ("n_iter", args.n_iter)) if v is not None}}
                if (args.batch or args.tol is not None or args.n_iter is not None) else {}),

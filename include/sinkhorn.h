@@ -92,8 +92,8 @@ SK_API size_t sinkhorn_workspace_bytes(const sk_problem *p);
  * d1 = d2 <= 104 that proves symmetric: K^T u = K u; any other C, shared or
  * per sample: both products); a problem whose scaled cost spans more than
  * 64 bits, or whose sums or scalings leave a guarded fp32 range at any
- * iteration, is re-solved from the start by the log-domain kernel launched
- * right after it on the same stream.  Every problem is solved: iters >= 0.
+ * iteration, is re-solved from the start in the log domain by the same
+ * work-group.  Every problem is solved: iters >= 0.
  *
  *   mu        [B, d1]              input histograms
  *   nu        [B, d2]
@@ -121,7 +121,7 @@ SK_API sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const fl
  *   SK_SELECT_LOG_ONLY       resident shapes: the log-domain kernel alone
  *                            (no plain-form attempt);
  *   SK_SELECT_PLAIN_ONLY     resident shapes: the first-choice plain-form
- *                            kernel alone, without the log-domain hand-over:
+ *                            kernel alone, without its log-domain fallback:
  *                            a problem it cannot keep in range comes back
  *                            with iters = -1 and its other outputs
  *                            unspecified;

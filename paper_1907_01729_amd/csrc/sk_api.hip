@@ -47,18 +47,21 @@ sk::BwdArgs bwd_args(const sk_problem *p, const float *grad_loss, const float *m
 // Resident regime.  First choice: the symmetric-cost kernel (shared cost,
 // d1 = d2 <= 104; it runs the general iteration in place when the cost is
 // not symmetric), else the general plain-form kernel (any cost).  Either
-// hands the problems it cannot keep in range to the log-domain kernel
-// (iters = -1), launched next on the same stream.  The selector of
-// sinkhorn_forward_select can pin one of these kernels.
-hipError_t launch_resident_regime(sk::FwdArgs a, hipStream_t s) {
+// solves the problems it cannot keep in range in the log domain, in place.
+// The selector of sinkhorn_forward_select can pin one of these kernels.
+hipError_t launch_resident_regime(const sk::FwdArgs &a, hipStream_t s) {
     if (a.select == SK_SELECT_LOG_ONLY) return sk::launch_resident(a, s);
     hipError_t e = hipSuccess;
     const bool ran = (a.select != SK_SELECT_NO_SYMMETRIC && sk::launch_resident_sym(a, s, &e)) ||
                      sk::launch_resident_gen(a, s, &e);
     if (!ran) return sk::launch_resident(a, s);
-    if (e != hipSuccess || a.select == SK_SELECT_PLAIN_ONLY) return e;
-    a.only_flagged = 1;
-    return sk::launch_resident(a, s);
+    // The widest bucket marks what it hands over; solve those problems next.
+    if (e == hipSuccess && a.select != SK_SELECT_PLAIN_ONLY && (a.d1 > 104 || a.d2 > 104)) {
+        sk::FwdArgs m = a;
+        m.only_marked = 1;
+        e = sk::launch_resident(m, s);
+    }
+    return e;
 }
 
 sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, const float *C, float *alpha,
@@ -80,8 +83,8 @@ sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, cons
     a.lambda = p->lambda;
     a.tol = p->tol;
     a.s = sk::kLog2eHost / p->lambda;
-    a.only_flagged = 0;
     a.select = SK_SELECT_DEFAULT;
+    a.only_marked = 0;
     return a;
 }
 

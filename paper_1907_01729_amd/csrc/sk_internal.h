@@ -18,12 +18,11 @@ struct FwdArgs {
     int B, d1, d2, n_iter, c_batched;
     float lambda, tol;
     float s;  // log2(e) / lambda
-    // Set (to 1) when a plain-form launch ran first: the log-domain kernel
-    // solves only the problems it marked with iters = -1 (out of the plain
-    // form's range) and leaves the others untouched.
-    int only_flagged;
     // Kernel selector of sinkhorn_forward_select (an sk_select value).
     int select;
+    // Set (to 1) for the log-domain launch that follows a plain-form launch of
+    // the widest bucket: it solves only the problems marked with iters = -1.
+    int only_marked;
 };
 
 struct BwdArgs {
@@ -34,14 +33,17 @@ struct BwdArgs {
     float s;  // log2(e) / lambda
 };
 
-// Largest support size the resident (one wavefront per problem) kernel takes.
+// Largest support size of the resident kernels (one work-group of two
+// wavefronts per problem, the cost in VGPRs).
 constexpr int kResidentMaxD = 128;
 
 bool resident_fits(int d1, int d2);
+// The log-domain kernel.
 hipError_t launch_resident(const FwdArgs &a, hipStream_t st);
 // Plain-form resident kernels: each returns false (and launches nothing) when
 // it does not take the shape; otherwise *err is the launch status.  Problems
-// it cannot keep in range come back with iters = -1.
+// it cannot keep in range are solved in the log domain by the same
+// work-group (left with iters = -1 under SK_SELECT_PLAIN_ONLY).
 // A shared cost with d1 = d2 <= 104, two wavefronts per problem
 // on the vector ALU.  On a cost that is not symmetric each work-group runs
 // the general kernel's iteration in place.

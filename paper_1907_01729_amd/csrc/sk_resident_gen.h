@@ -12,8 +12,8 @@
 // u^0 = 1 on the support of mu, with the range guards of the symmetric
 // kernel: a cost spread over more than 64 bits, or a sum R_i, S_j outside
 // [2^-64, 2^64] or a scaling outside [2^-100, 2^100] on the supports in any
-// iteration, marks the problem with iters = -1 for the log-domain kernel
-// (the guard flags are kept per lane and exchanged once, after the loop).
+// iteration, hands the problem to the log-domain iteration (the guard flags
+// are kept per lane and exchanged once, after the loop).
 // Outputs alpha = ln2 log2 U, beta = ln2 (log2 V - clmax): the potentials of
 // the log-domain iterates up to rounding.
 //
@@ -80,8 +80,10 @@ static_assert(kGenRowv % 4 == 0 && kGenCp % 4 == 0 && kGenTsum % 4 == 0 && kGenR
 // One problem (b = blockIdx.x) per work-group of 128 threads.  Every
 // thread of the work-group calls it, from wavefront-uniform control flow;
 // pool: kGenLdsFloats floats of LDS, 16-byte aligned, contents irrelevant.
+// Returns true (on every thread, nothing written) when the problem leaves the
+// plain form's range: the caller then solves it in the log domain.
 template <int N>
-__device__ __forceinline__ void resident_gen_body(const FwdArgs &A, float *pool) {
+__device__ __forceinline__ bool resident_gen_body(const FwdArgs &A, float *pool) {
     constexpr int H = (N + 1) / 2;
     static_assert(8 * N <= 128 && H <= 8, "one thread per column, one lane per row");
     // V[j] at colv[(j & 7) * kVS + (j >> 3)] (lane (p, q) reads line q);
@@ -149,8 +151,7 @@ __device__ __forceinline__ void resident_gen_body(const FwdArgs &A, float *pool)
     const float clmax = -s * fminf(ini[0][1], ini[1][1]);
     const float clmin = -s * fmaxf(ini[0][2], ini[1][2]);
     if (ini[0][0] + ini[1][0] != 0.f || !(clmax - clmin <= kRangeBits)) {  // a non-finite cost fails too
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+        return true;
     }
     // K on the cells of the problem, 0 elsewhere.
 #pragma unroll
@@ -181,8 +182,7 @@ __device__ __forceinline__ void resident_gen_body(const FwdArgs &A, float *pool)
     if (rown) rowv[rslot] = ms > 0.f ? 1.f : 0.f;
     __syncthreads();
     if (ini[0][3] + ini[1][3] == 0.f || red[0][0][0] + red[0][1][0] == 0.f) {  // empty support
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+        return true;
     }
 
     // The FMAs of both products run at the lowest issue priority and the rest
@@ -293,8 +293,7 @@ __device__ __forceinline__ void resident_gen_body(const FwdArgs &A, float *pool)
     if (kstop != n_iter && c < 8 * N) colv[cslot] = V;
     __syncthreads();
     if (ini[0][0] + ini[1][0] != 0.f) {
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return;
+        return true;
     }
     float err, lsum;
     {
@@ -344,6 +343,7 @@ __device__ __forceinline__ void resident_gen_body(const FwdArgs &A, float *pool)
         A.marg_err[b] = red[0][0][0] + red[0][1][0];
         A.iters[b] = kstop;
     }
+    return false;
 }
 
 }  // namespace

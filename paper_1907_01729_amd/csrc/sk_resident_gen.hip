@@ -1,15 +1,15 @@
 // sk_resident_gen.hip -- any cost (shared by the batch or one per problem)
 // with max(d1, d2) <= 128: the general plain-form kernel, one work-group of
 // two wavefronts per problem (the iteration itself is in sk_resident_gen.h).
-#include "sk_resident_gen.h"
+#include "sk_resident_log.h"
 
 namespace sk {
 namespace {
 
 template <int N>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void sk_resident_gen_kernel(FwdArgs A) {
-    __shared__ __attribute__((aligned(16))) float pool[kGenLdsFloats];
-    resident_gen_body<N>(A, pool);
+    __shared__ __attribute__((aligned(16))) float pool[kGenLdsFloats > kLogLdsFloats ? kGenLdsFloats : kLogLdsFloats];
+    if (resident_gen_body<N>(A, pool)) hand_over_to_log<N>(A, pool);
 }
 
 template <int N>

@@ -30,7 +30,7 @@
 // spread wider than the range at the start, or a guard that failed in any
 // iteration (checked once, at the end): a sum R_i, S_j outside
 // [2^-64, 2^64] or a scaling U_i, V_j outside [2^-100, 2^100] on the supports.
-#include "sk_resident_gen.h"  // the general iteration, the range guards
+#include "sk_resident_log.h"  // the general iteration, the range guards
 
 namespace sk {
 namespace {
@@ -72,7 +72,8 @@ constexpr int LDC = 136;
 constexpr int oXs = 0, oTsum = oXs + 2 * 8 * XS, oCst = oTsum + 2 * kRowTotalsFloats, oRed = oCst + 2 * 8 * LDC,
               oIni = oRed + 8, kSymLdsFloats = oIni + 16;
 static_assert(oTsum % 4 == 0 && oCst % 4 == 0 && oRed % 4 == 0, "16-byte offsets");
-constexpr int kSymPoolFloats = kSymLdsFloats > kGenLdsFloats ? kSymLdsFloats : kGenLdsFloats;
+constexpr int kSymPoolFloats = kSymLdsFloats > kGenLdsFloats ? (kSymLdsFloats > kLogLdsFloats ? kSymLdsFloats : kLogLdsFloats)
+                                                              : (kGenLdsFloats > kLogLdsFloats ? kGenLdsFloats : kLogLdsFloats);
 
 // Work-group = one problem, two wavefronts: wavefront W holds H row blocks
 // from R0 on (ceil(NC / 2) for the first, floor(NC / 2) for the second, so no
@@ -82,10 +83,14 @@ constexpr int kSymPoolFloats = kSymLdsFloats > kGenLdsFloats ? kSymLdsFloats : k
 // one problem per SIMD: a single wavefront issues a vector instruction only
 // every few cycles, two interleave.  The two wavefronts run separate
 // instantiations (W = 0, 1) of this body, which pass the same barriers.
-// Returns true, for both wavefronts and after a barrier that frees the LDS
-// pool, when the cost is not symmetric (nothing written); false otherwise.
+// Returns, the same on both wavefronts: kSymAsym after a barrier that frees
+// the LDS pool when the cost is not symmetric (nothing written);
+// kSymHandOver when the problem leaves the plain form's range (nothing
+// written); kSymDone otherwise.
+constexpr int kSymDone = 0, kSymAsym = 1, kSymHandOver = 2;
+
 template <int NC, int W>
-__device__ __forceinline__ bool sym_body(const FwdArgs &A, float *pool) {
+__device__ __forceinline__ int sym_body(const FwdArgs &A, float *pool) {
     constexpr int H = W == 0 ? (NC + 1) / 2 : NC / 2;
     constexpr int R0 = W == 0 ? 0 : (NC + 1) / 2;
     static_assert(R0 + H <= XS, "row blocks per column-block line");
@@ -186,14 +191,13 @@ __device__ __forceinline__ bool sym_body(const FwdArgs &A, float *pool) {
     __syncthreads();
     if (ini[0][0][0] + ini[0][1][0] != 0.f) {  // the same verdict for every problem: the cost is shared
         __syncthreads();  // every thread has read the verdict: the pool is free
-        return true;
+        return kSymAsym;
     }
     // Raw cost range -> cl range (cl = -s C with s > 0: the extremes swap).
     const float clmax = -s * fminf(ini[0][0][2], ini[0][1][2]);
     const float clmin = -s * fmaxf(ini[0][0][3], ini[0][1][3]);
     if (ini[0][0][1] + ini[0][1][1] != 0.f || !(clmax - clmin <= kRangeBits)) {  // a non-finite cost fails too
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return false;
+        return kSymHandOver;
     }
     // K on the cells of the problem; elsewhere a finite value in (0, 1]
     // (the clamp), which meets only zero operands and unused rows.
@@ -221,8 +225,7 @@ __device__ __forceinline__ bool sym_body(const FwdArgs &A, float *pool) {
     if (own) xs[0][xl] = ms > 0.f ? 1.f : 0.f;
     __syncthreads();
     if (ini[1][0][0] + ini[1][1][0] == 0.f || ini[1][0][1] + ini[1][1][1] == 0.f) {  // empty support
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return false;
+        return kSymHandOver;
     }
 
     const int n_iter = A.n_iter;
@@ -321,8 +324,7 @@ __device__ __forceinline__ bool sym_body(const FwdArgs &A, float *pool) {
     if (own) xs[1][xl] = V;
     __syncthreads();
     if (ini[0][0][0] + ini[0][1][0] != 0.f) {
-        if (threadIdx.x == 0) A.iters[b] = -1;
-        return false;
+        return kSymHandOver;
     }
     gather_lds(xs[1]);
     X = kmul<H, NC>(K, wc, tb, p, q);  // row sums R = K V
@@ -366,15 +368,17 @@ __device__ __forceinline__ bool sym_body(const FwdArgs &A, float *pool) {
         A.marg_err[b] = red[0][0][0] + red[0][1][0];
         A.iters[b] = kstop;
     }
-    return false;
+    return kSymDone;
 }
 
 template <int NC>
 __global__ __launch_bounds__(128) void sk_resident_sym_kernel(FwdArgs A) {
     __shared__ __attribute__((aligned(16))) float pool[kSymPoolFloats];
-    const bool asym = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0 ? sym_body<NC, 0>(A, pool)
-                                                                            : sym_body<NC, 1>(A, pool);
-    if (asym) resident_gen_body<NC>(A, pool);  // the general iteration in place (its own reads of the cost)
+    int r = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0 ? sym_body<NC, 0>(A, pool)
+                                                                   : sym_body<NC, 1>(A, pool);
+    // the general iteration in place (its own reads of the cost)
+    if (r == kSymAsym) r = resident_gen_body<NC>(A, pool) ? kSymHandOver : kSymDone;
+    if (r == kSymHandOver) hand_over_to_log<NC>(A, pool);
 }
 
 template <int NC>

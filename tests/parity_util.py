@@ -40,3 +40,14 @@ def rel_err_rows(x, ref):
 def loss_rel_err(loss, ref):
     ref = np.asarray(ref, dtype=np.float64)
     return float(np.max(np.abs(np.asarray(loss, dtype=np.float64) - ref) / np.maximum(np.abs(ref), 1e-30)))
+
+
+def max_abs_rel_rows(x, ref):
+    """max over samples of max|x_b - ref_b| / max|ref_b| (flattened per sample):
+    the elementwise companion of rel_err_rows."""
+    x = np.asarray(x, dtype=np.float64).reshape(ref.shape[0], -1)
+    ref = np.asarray(ref, dtype=np.float64).reshape(ref.shape[0], -1)
+    num = np.max(np.abs(x - ref), axis=1)
+    den = np.max(np.abs(ref), axis=1)
+    den = np.where(den > 0, den, 1.0)
+    return float(np.max(num / den))
