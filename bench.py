@@ -134,14 +134,14 @@ def cpu_baseline(prob, grad_C, sharp=False):
                        f"{' (gradient of E^0, dense solve)' if sharp else ''}, {passes} passes, {dt:.2f} s")
 
 
-def cpu_baseline_sampled(prob, grad_C, n_samples):
+def cpu_baseline_sampled(prob, grad_C, n_samples, sharp=False):
     import oracle
     import workloads
 
     idx = np.arange(n_samples)
     C = prob.C[idx] if prob.c_batched else prob.C
     sub = workloads.Problem(prob.name, prob.mu[idx], prob.nu[idx], C, prob.lam, prob.n_iter, prob.tol, grad_C)
-    r = cpu_baseline(sub, grad_C)
+    r = cpu_baseline(sub, grad_C, sharp=sharp)
     r["sample"] = (f"first {n_samples} of {prob.B} problems of workload {prob.name}, one forward+backward "
                    f"({', '.join(r['sample'].split(', ')[-2:])})")
     return r
@@ -212,8 +212,8 @@ def main():
     import workloads
 
     points = args.config == 6
-    if args.sharp and args.config not in (1, 2):
-        print("bench.py: --sharp takes configs 1 and 2 (max(d1, d2) <= 128)", file=sys.stderr)
+    if args.sharp and args.config not in (1, 2, 3):
+        print("bench.py: --sharp takes configs 1, 2 and 3", file=sys.stderr)
         sys.exit(2)
     over = {"B": args.batch} if args.batch else {}
     prob = workloads.clouds_points(**over) if points else workloads.make_config(args.config, **over)
@@ -426,7 +426,8 @@ def main():
         elif args.config in (1, 2):
             res["cpu_baseline"] = cpu_baseline(prob, grad_C, sharp=args.sharp)
         else:
-            res["cpu_baseline"] = cpu_baseline_sampled(prob, grad_C, {3: 16, 4: 1, 5: 2}[args.config])
+            res["cpu_baseline"] = cpu_baseline_sampled(prob, grad_C, {3: 2 if args.sharp else 16, 4: 1, 5: 2}[args.config],
+                                                       sharp=args.sharp)
     print(json.dumps(res), flush=True)
 
 

@@ -207,15 +207,26 @@ SK_API sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss,
  * projected off that direction.  Solved per problem by conjugate gradients
  * preconditioned with (r, c): at most max_cg (>= 1) iterations, stopping when
  * the preconditioned residual norm falls below cg_tol (>= 0) times its start
- * value.  Shapes: max(d1, d2) <= 128 (SK_ERR_SHAPE otherwise).  cg_iters
- * [B] int32 (may be NULL) receives the iterations taken.  Needs no
- * workspace; deterministic.  Invalid max_cg or cg_tol: SK_ERR_ITERS.
+ * value.  cg_iters [B] int32 (may be NULL) receives the iterations taken.
+ * For max(d1, d2) <= 128 the plan of a problem sits in the registers of one
+ * work-group and no workspace is needed (workspace may be NULL); larger
+ * supports (the shapes sinkhorn_forward takes in its tiled regime) rebuild the
+ * plan from (alpha, beta, C) in a sweep over the cost for every product and
+ * keep the iteration's vectors in a workspace of at least
+ * sinkhorn_sharp_workspace_bytes(p) bytes (SK_ERR_WORKSPACE if smaller); every
+ * problem then runs max_cg launches of which those after its convergence do
+ * nothing.  Deterministic.  Invalid max_cg or cg_tol: SK_ERR_ITERS.
  */
 SK_API sk_status sinkhorn_backward_sharp(const sk_problem *p, const float *grad_loss,
                                   const float *mu, const float *nu, const float *C,
                                   const float *alpha, const float *beta, float *grad_mu,
                                   float *grad_nu, int32_t max_cg, float cg_tol,
-                                  int32_t *cg_iters, void *stream);
+                                  int32_t *cg_iters, void *workspace, size_t ws_bytes,
+                                  void *stream);
+
+/* Bytes of workspace sinkhorn_backward_sharp needs for *p (0 when the
+ * problem needs none, and for an invalid problem). */
+SK_API size_t sinkhorn_sharp_workspace_bytes(const sk_problem *p);
 
 /*
  * Point clouds.  The cost is the squared Euclidean distance between points,

@@ -37,6 +37,7 @@ EXPORTED = (
     "sinkhorn_forward_points",
     "sinkhorn_backward_points",
     "sinkhorn_backward_sharp",
+    "sinkhorn_sharp_workspace_bytes",
 )
 
 
@@ -95,8 +96,10 @@ def load_library():
     lib.sinkhorn_forward_points.restype = ctypes.c_int
     lib.sinkhorn_backward_points.argtypes = [PP, I, P, P, P, P, P, P, P, P, P, P, P, P]
     lib.sinkhorn_backward_points.restype = ctypes.c_int
-    lib.sinkhorn_backward_sharp.argtypes = [PP, P, P, P, P, P, P, P, P, I, ctypes.c_float, P, P]
+    lib.sinkhorn_backward_sharp.argtypes = [PP, P, P, P, P, P, P, P, P, I, ctypes.c_float, P, P, ctypes.c_size_t, P]
     lib.sinkhorn_backward_sharp.restype = ctypes.c_int
+    lib.sinkhorn_sharp_workspace_bytes.argtypes = [PP]
+    lib.sinkhorn_sharp_workspace_bytes.restype = ctypes.c_size_t
     _lib = lib
     return lib
 
@@ -328,7 +331,13 @@ def sinkhorn_backward_points(grad_loss, mu, nu, X, Y, lam, alpha, beta, grad_poi
     return out
 
 
-def sinkhorn_backward_sharp(grad_loss, mu, nu, C, lam, alpha, beta, max_cg=200, cg_tol=1e-6, stream=None):
+def sinkhorn_sharp_workspace_bytes(B, d1, d2, c_batched, lam=1.0) -> int:
+    p = problem(B, d1, d2, c_batched, lam, 0, 0.0)
+    return int(load_library().sinkhorn_sharp_workspace_bytes(ctypes.byref(p)))
+
+
+def sinkhorn_backward_sharp(grad_loss, mu, nu, C, lam, alpha, beta, max_cg=200, cg_tol=1e-6, stream=None,
+                            workspace=None):
     """Gradient of the sharp loss E^0 itself (implicit differentiation of the
     plan, conjugate gradients per problem): dict(grad_mu, grad_nu, cg_iters)."""
     lib = load_library()
@@ -342,9 +351,13 @@ def sinkhorn_backward_sharp(grad_loss, mu, nu, C, lam, alpha, beta, max_cg=200, 
         gmu = torch.empty((B, d1), **f)
         gnu = torch.empty((B, d2), **f)
         its = torch.empty((B,), device=dev, dtype=torch.int32)
+        need = int(lib.sinkhorn_sharp_workspace_bytes(ctypes.byref(p)))
+        if workspace is None or workspace.numel() < need:
+            workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
     st = lib.sinkhorn_backward_sharp(ctypes.byref(p), _ptr(grad_loss), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
                                      _ptr(beta), _ptr(gmu), _ptr(gnu), int(max_cg), ctypes.c_float(cg_tol),
-                                     _ptr(its), _stream(dev, stream))
+                                     _ptr(its), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+                                     _stream(dev, stream))
     if st != 0:
         raise SinkhornError(st, "sinkhorn_backward_sharp")
     return dict(grad_mu=gmu, grad_nu=gnu, cg_iters=its)

@@ -231,15 +231,27 @@ sk_status sinkhorn_backward(const sk_problem *p, const float *grad_loss, const f
     return e == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 
+size_t sinkhorn_sharp_workspace_bytes(const sk_problem *p) {
+    if (check_problem(p) != SK_OK) return 0;
+    if (p->d1 <= sk::kSharpMaxD && p->d2 <= sk::kSharpMaxD) return 0;
+    if (!sk::sharp_tiled_fits(p->B, p->d1, p->d2)) return 0;
+    return sk::sharp_tiled_workspace_bytes(p->B, p->d1, p->d2);
+}
+
 sk_status sinkhorn_backward_sharp(const sk_problem *p, const float *grad_loss, const float *mu, const float *nu,
                                   const float *C, const float *alpha, const float *beta, float *grad_mu,
-                                  float *grad_nu, int32_t max_cg, float cg_tol, int32_t *cg_iters, void *stream) {
+                                  float *grad_nu, int32_t max_cg, float cg_tol, int32_t *cg_iters, void *workspace,
+                                  size_t ws_bytes, void *stream) {
     sk_status st = check_problem(p);
     if (st != SK_OK) return st;
-    if (p->d1 > sk::kSharpMaxD || p->d2 > sk::kSharpMaxD) return SK_ERR_SHAPE;
+    const bool resident = p->d1 <= sk::kSharpMaxD && p->d2 <= sk::kSharpMaxD;
+    if (!resident && !sk::sharp_tiled_fits(p->B, p->d1, p->d2)) return SK_ERR_SHAPE;
     if (max_cg < 1 || !(cg_tol >= 0.f) || !isfinite(cg_tol)) return SK_ERR_ITERS;
     if (p->B == 0) return SK_OK;
     if (!grad_loss || !mu || !nu || !C || !alpha || !beta || !grad_mu || !grad_nu) return SK_ERR_NULLPTR;
+    const size_t need = sinkhorn_sharp_workspace_bytes(p);
+    if (ws_bytes < need) return SK_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return SK_ERR_NULLPTR;
     sk::SharpArgs a;
     a.grad_loss = grad_loss;
     a.mu = mu;
@@ -257,7 +269,9 @@ sk_status sinkhorn_backward_sharp(const sk_problem *p, const float *grad_loss, c
     a.max_cg = max_cg;
     a.s = sk::kLog2eHost / p->lambda;
     a.cg_tol = cg_tol;
-    return sk::launch_sharp(a, static_cast<hipStream_t>(stream)) == hipSuccess ? SK_OK : SK_ERR_HIP;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const hipError_t e = resident ? sk::launch_sharp(a, s) : sk::launch_sharp_tiled(a, workspace, s);
+    return e == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 
 sk_status sinkhorn_forward_points(const sk_problem *p, int32_t D, const float *mu, const float *nu, const float *X,

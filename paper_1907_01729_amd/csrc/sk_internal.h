@@ -73,6 +73,11 @@ struct SharpArgs {
     float cg_tol;
 };
 hipError_t launch_sharp(const SharpArgs &a, hipStream_t st);
+// Larger supports: the plan rebuilt in sweeps over the cost for every
+// product, the conjugate-gradient vectors in a workspace.
+bool sharp_tiled_fits(int B, int d1, int d2);
+size_t sharp_tiled_workspace_bytes(int B, int d1, int d2);
+hipError_t launch_sharp_tiled(const SharpArgs &a, void *ws, hipStream_t st);
 
 // Point clouds (C_ij = sum_k (x_ik - y_jk)^2).  The tiled sweep computes the
 // cost on the fly for per-sample clouds with up to kPointsMaxD coordinates

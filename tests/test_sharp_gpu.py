@@ -104,12 +104,59 @@ def test_sharp_iteration_cap_and_deterministic():
         np.testing.assert_array_equal(a[k].cpu().numpy(), b[k].cpu().numpy())
 
 
-def test_sharp_rejects_large_shapes():
-    prob = workloads.random_problem(seed=43, B=2, d1=129, d2=20, lam=0.1, n_iter=5)
+def test_sharp_tiled_image_sampled():
+    """Image histograms (28 x 28 grid, d = 784, lambda = 0.01, 300
+    iterations; B = 16): larger than a work-group's registers, so every
+    product rebuilds the plan in a sweep over the cost.  The dense solve on
+    three problems."""
+    prob = workloads.make_config(3, B=16)
+    check_sharp(prob, idx=np.array([0, 7, 15]), max_cg=1000)
+
+
+def test_sharp_tiled_per_sample_ragged_zero_masses():
+    """Per-sample costs, 300 x 520 (a ragged last column block), zero masses:
+    gradients exactly 0 off the supports."""
+    prob = workloads.random_problem(seed=45, B=3, d1=300, d2=520, lam=0.1, n_iter=300, c_batched=True,
+                                    zero_frac=0.1)
+    assert (prob.mu == 0).any() and (prob.nu == 0).any()
+    out, _ = check_sharp(prob, max_cg=1000)
+    assert np.all(out["grad_mu"].cpu().numpy()[prob.mu == 0] == 0)
+    assert np.all(out["grad_nu"].cpu().numpy()[prob.nu == 0] == 0)
+
+
+@pytest.mark.parametrize("d1,d2", [(129, 7), (9, 600), (250, 4096)])
+def test_sharp_tiled_shapes(d1, d2):
+    prob = workloads.random_problem(seed=500 + d1 + d2, B=2, d1=d1, d2=d2, lam=0.2, n_iter=200)
+    check_sharp(prob, max_cg=1000)
+
+
+def test_sharp_tiled_against_converged_oracle():
+    """Both forwards converged (3000 iterations, lambda = 0.2): the GPU's sharp
+    gradient from its own forward matches the oracle's from its own."""
+    prob = workloads.random_problem(seed=46, B=2, d1=150, d2=200, lam=0.2, n_iter=3000)
     mu, nu, C = _t(prob.mu), _t(prob.nu), _t(prob.C)
     fw = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter)
-    with pytest.raises(sk.SinkhornError):
-        sk.sinkhorn_backward_sharp(torch.ones(2, device=DEV), mu, nu, C, prob.lam, fw["alpha"], fw["beta"])
+    g = torch.ones(prob.B, device=DEV)
+    out = sk.sinkhorn_backward_sharp(g, mu, nu, C, prob.lam, fw["alpha"], fw["beta"], max_cg=1000)
+    o = oracle.forward(prob.mu, prob.nu, prob.C, prob.lam, prob.n_iter)
+    ref = oracle.sharp_gradient(np.ones(prob.B), prob.mu, prob.nu, prob.C, prob.lam, o["alpha"], o["beta"])
+    e1 = rel_err_rows(out["grad_mu"].cpu().numpy(), ref["grad_mu"])
+    e2 = rel_err_rows(out["grad_nu"].cpu().numpy(), ref["grad_nu"])
+    _say(f"   converged tiled: grad_mu {e1:.2e} grad_nu {e2:.2e} cg {out['cg_iters'].cpu().numpy().tolist()}")
+    assert e1 <= GRAD_RTOL and e2 <= GRAD_RTOL
+
+
+def test_sharp_tiled_iteration_cap_and_deterministic():
+    prob = workloads.random_problem(seed=47, B=3, d1=200, d2=150, lam=0.1, n_iter=100)
+    mu, nu, C = _t(prob.mu), _t(prob.nu), _t(prob.C)
+    fw = sk.sinkhorn_forward(mu, nu, C, prob.lam, prob.n_iter)
+    g = torch.ones(prob.B, device=DEV)
+    capped = sk.sinkhorn_backward_sharp(g, mu, nu, C, prob.lam, fw["alpha"], fw["beta"], max_cg=3, cg_tol=0.0)
+    assert np.all(capped["cg_iters"].cpu().numpy() == 3)
+    a = sk.sinkhorn_backward_sharp(g, mu, nu, C, prob.lam, fw["alpha"], fw["beta"], max_cg=500)
+    b = sk.sinkhorn_backward_sharp(g, mu, nu, C, prob.lam, fw["alpha"], fw["beta"], max_cg=500)
+    for k in a:
+        np.testing.assert_array_equal(a[k].cpu().numpy(), b[k].cpu().numpy())
 
 
 def test_sharp_autograd_wrapper():
