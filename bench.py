@@ -42,9 +42,12 @@ PEAK_FP32_VALU = 157.3
 # symmetric cost with d1 = d2 <= 104: the symmetric kernel; any other cost
 # (shared or per sample): the general kernel.
 RESIDENT_KERNELS = {
-    "sym": ("sk_resident_sym_kernel", ("sk_resident_sym.hip", "sk_resident_gen.h"), "alu", PEAK_FP32_VALU),
-    "shared": ("sk_resident_gen_kernel", ("sk_resident_gen.hip", "sk_resident_gen.h"), "alu", PEAK_FP32_VALU),
-    "batched": ("sk_resident_gen_kernel", ("sk_resident_gen.hip", "sk_resident_gen.h"), "alu", PEAK_FP32_VALU),
+    "sym": ("sk_resident_sym_kernel", ("sk_resident_sym.hip", "sk_resident_gen.h", "sk_resident_log.h"), "alu",
+            PEAK_FP32_VALU),
+    "shared": ("sk_resident_gen_kernel", ("sk_resident_gen.hip", "sk_resident_gen.h", "sk_resident_log.h"), "alu",
+               PEAK_FP32_VALU),
+    "batched": ("sk_resident_gen_kernel", ("sk_resident_gen.hip", "sk_resident_gen.h", "sk_resident_log.h"), "alu",
+                PEAK_FP32_VALU),
 }
 
 
