@@ -74,11 +74,22 @@ WORKLOAD_NAMES = {
 }
 
 
+def code_text(src):
+    """Source text without comments, trailing blanks and empty lines: what
+    compiles into the kernel (string literals in these files hold no comment
+    markers)."""
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    lines = (re.sub(r"//.*$", "", l).rstrip() for l in src.splitlines())
+    return "\n".join(l for l in lines if l)
+
+
 def kernel_source_hash(files):
+    """Hash of the kernel sources' code (comments and blank lines excluded), the
+    key under which a committed counter summary holds for the current kernel."""
     h = hashlib.sha256()
     for f in files:
-        with open(os.path.join(ROOT, "paper_1907_01729_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_1907_01729_amd", "csrc", f)) as fh:
+            h.update(code_text(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -9,9 +9,11 @@
 //     updated plan in registers                           -> column partials.
 // (One exponential per cell per iteration; see the resident kernel for why the
 // current potential is a valid logsumexp shift.)  Column partials of a
-// work-group's wavefronts are combined in LDS, the row blocks' partials are
-// merged by a separate kernel in a fixed order (no float atomics), which also
-// performs the v-update and the column part of the marginal error.
+// work-group's wavefronts are combined in LDS; the row blocks' partials are
+// summed in a fixed order (no float atomics) by one work-group per problem
+// (sk_tiled_merge_cols), which also performs the v-update and takes the
+// marginal error.  The streaming sweep (per-sample cost) folds that merge into
+// the start of the next sweep instead.
 //
 // Launch sequence for n iterations:
 //   init                 a^0 = 0 on supp(mu), -inf off it; stop flags cleared
@@ -21,11 +23,12 @@
 //   sweep(k), merge(k)   k = 1..n (no merge after the last sweep)
 //   sweep(stats), final  loss E^0 and marginal error of the returned iterate,
 //                        outputs in natural-log units
-// Early stop (tol > 0): sweep(k+1) sums the row-block and column-chunk error
-// partials of iterate k in a fixed order; every work-group of a problem takes
-// the same decision, and the first row block records K = k in the stop flag,
-// which later sweeps and merges honour.  Row-error partials are double
-// buffered so a decision never reads a partial being rewritten.
+// Early stop (tol > 0): the merge of problem b holds b's whole error after
+// iteration k (column part summed there, row part from the sweep's
+// double-buffered row-block partials) and records K = k in the stop flag,
+// which every later sweep and merge honours.  In the streaming sweep every
+// work-group of b sums the same partials in the same order, so all take the
+// same decision, and the first row block records it.
 #include "sk_device.h"
 #include "sk_internal.h"
 
