@@ -201,7 +201,7 @@ def main():
                          "'log' times the log-domain kernel alone); the line names it")
     ap.add_argument("--sharp", action="store_true",
                     help="backward = gradient of E^0 itself (implicit differentiation, conjugate gradients; "
-                         "resident shapes: configs 1 and 2)")
+                         "configs 1, 2 and 3)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 3 times (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
