@@ -54,6 +54,37 @@ bool launch_resident_gen(const FwdArgs &a, hipStream_t st, hipError_t *err);
 
 // The tiled sweep keeps a whole cost row in one wavefront's registers.
 constexpr int kTiledMaxD2 = 4096;
+// The tiled kernels carry the batch on a grid dimension of at most 65535
+// work-groups: a larger batch runs as consecutive chunks of at most that
+// many problems (the problems are independent), each chunk reusing the
+// workspace of the largest one in stream order.
+constexpr int kTiledMaxBatch = 65535;
+inline int tiled_chunk(int B) { return B < kTiledMaxBatch ? B : kTiledMaxBatch; }
+// The arguments of problems [off, off + n) of a forward.
+inline FwdArgs fwd_chunk(const FwdArgs &a, int off, int n) {
+    FwdArgs c = a;
+    const size_t o1 = (size_t)off * a.d1, o2 = (size_t)off * a.d2;
+    c.mu += o1;
+    c.alpha += o1;
+    c.nu += o2;
+    c.beta += o2;
+    if (a.C && a.c_batched) c.C += o1 * a.d2;
+    c.loss += off;
+    c.marg_err += off;
+    c.iters += off;
+    c.B = n;
+    return c;
+}
+// Runs launch(off, n) over the chunks of a batch of B problems, stopping at
+// the first error.
+template <class Launch>
+hipError_t for_each_chunk(int B, Launch launch) {
+    for (int off = 0; off < B; off += kTiledMaxBatch) {
+        const hipError_t e = launch(off, B - off < kTiledMaxBatch ? B - off : kTiledMaxBatch);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
 bool tiled_fits(int B, int d1, int d2, int c_batched);
 size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched);
 hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);

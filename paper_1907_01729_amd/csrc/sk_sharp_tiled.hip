@@ -385,20 +385,8 @@ hipError_t run_sht(const ShtArgs &T, hipStream_t st) {
     return hipGetLastError();
 }
 
-}  // namespace
-
-size_t sharp_tiled_workspace_bytes(int B, int d1, int d2) {
-    int R, RBS, d2p;
-    return sht_layout(B, d1, d2, &R, &RBS, &d2p).total;
-}
-
-bool sharp_tiled_fits(int B, int d1, int d2) {
-    int R, RBS;
-    sht_row_blocks(B, d1, &R, &RBS);
-    return d2 <= kTiledMaxD2 && B <= 65535 && R <= 65535;
-}
-
-hipError_t launch_sharp_tiled(const SharpArgs &a, void *ws, hipStream_t st) {
+// One chunk (at most kTiledMaxBatch problems) of the solve.
+hipError_t launch_sharp_tiled_chunk(const SharpArgs &a, void *ws, hipStream_t st) {
     ShtArgs T;
     int R, RBS, d2p;
     const ShtLayout L = sht_layout(a.B, a.d1, a.d2, &R, &RBS, &d2p);
@@ -443,6 +431,42 @@ hipError_t launch_sharp_tiled(const SharpArgs &a, void *ws, hipStream_t st) {
         case 32: return run_sht<32>(T, st);
         default: return run_sht<64>(T, st);
     }
+}
+
+}  // namespace
+
+size_t sharp_tiled_workspace_bytes(int B, int d1, int d2) {
+    int R, RBS, d2p;
+    return sht_layout(tiled_chunk(B), d1, d2, &R, &RBS, &d2p).total;
+}
+
+bool sharp_tiled_fits(int B, int d1, int d2) {
+    int R, RBS;
+    sht_row_blocks(tiled_chunk(B), d1, &R, &RBS);
+    if (R > 65535) return false;
+    if (B > kTiledMaxBatch && B % kTiledMaxBatch) {
+        sht_row_blocks(B % kTiledMaxBatch, d1, &R, &RBS);
+        if (R > 65535) return false;
+    }
+    return d2 <= kTiledMaxD2;
+}
+
+hipError_t launch_sharp_tiled(const SharpArgs &a, void *ws, hipStream_t st) {
+    return for_each_chunk(a.B, [&](int off, int n) {
+        SharpArgs c = a;
+        const size_t o1 = (size_t)off * a.d1, o2 = (size_t)off * a.d2;
+        c.grad_loss += off;
+        c.mu += o1;
+        c.alpha += o1;
+        c.grad_mu += o1;
+        c.nu += o2;
+        c.beta += o2;
+        c.grad_nu += o2;
+        if (a.c_batched) c.C += o1 * a.d2;
+        if (a.cg_iters) c.cg_iters += off;
+        c.B = n;
+        return launch_sharp_tiled_chunk(c, ws, st);
+    });
 }
 
 }  // namespace sk

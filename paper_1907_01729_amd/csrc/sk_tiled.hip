@@ -437,6 +437,123 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_sweep(TiledArgs T, int k) {
     }
 }
 
+// ---- Rows wider than one wavefront's registers hold (d2 > kTiledMaxD2) ----
+//
+// The one-pass sweeps keep a row's plan entries in registers between its row
+// sum and its column sums.  A wider row takes two passes per iteration over
+// the cost, one exponential per cell in each, with the same shifted sums and
+// exact fallbacks (so the same iterates):
+//   sk_wide_rows  one wavefront per row, looping over the columns: the row
+//                 sum of the plan after the last v-update, the u-update in
+//                 place, the row part of the marginal error;
+//   sk_wide_cols  one thread per column, looping over a row block: the column
+//                 partials of the plan after that u-update, merged by
+//                 sk_tiled_merge_cols like every other sweep's.
+// STATS: the plan of the returned iterate, without update (row error and
+// loss partials, column partials) for sk_tiled_final.
+constexpr int kWideRowWaves = 16;  // rows kernel: 16 wavefronts, one row each at a time
+
+template <bool STATS>
+__global__ __launch_bounds__(64 * kWideRowWaves) void sk_wide_rows(TiledArgs T, int k) {
+    __shared__ float scal[2 * kWideRowWaves];
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int st = T.state[b];
+    if (!STATS && st != 0) return;  // stopped by an earlier merge's test (block-uniform)
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+    const int d1 = T.d1, d2 = T.d2;
+    const float s = T.s;
+    const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
+    const float *Cb = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0);
+    float *ab = T.a + (size_t)b * d1;
+    const float *mub = T.mu + (size_t)b * d1;
+    float rowerr = 0.f, losspart = 0.f;  // rowerr wavefront-uniform, losspart per lane
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    for (int i = i0 + w; i < i1; i += kWideRowWaves) {
+        const float mui = mub[i];
+        if (!STATS && !(mui > 0.f)) continue;  // zero-mass row: a_i = -inf, its entries 0
+        const float ai = ab[i];
+        const float *row = Cb + (size_t)i * d2;
+        float acc = 0.f;
+        for (int j = lane; j < d2; j += 64) {
+            const float cl = -s * row[j];
+            const float v = ex2((ai + bsrc[j]) + cl);
+            acc += v;
+            if (STATS) losspart = __builtin_fmaf(v, cl, losspart);
+        }
+        const float rs = wave_sum(acc);
+        if (STATS) {
+            if (mui > 0.f) rowerr += fabsf(rs - mui);
+            continue;
+        }
+        const float lmu = log2f(mui);
+        float an;
+        if (rs >= kSumLo && rs <= kSumHi) {
+            an = ai + lmu - lg2(rs);
+            rowerr += fabsf(ex2(an - ai) * rs - mui);
+        } else {
+            // Exact u-update of this row (max, then sum); the row error from
+            // the entries rebuilt with the new potential.
+            float m = neg_inf();
+            for (int j = lane; j < d2; j += 64) m = fmaxf(m, bsrc[j] - s * row[j]);
+            m = wave_max(m);
+            float s2 = 0.f;
+            for (int j = lane; j < d2; j += 64) s2 += ex2(bsrc[j] - s * row[j] - m);
+            an = lmu - (m + lg2(wave_sum(s2)));
+            float s3 = 0.f;
+            for (int j = lane; j < d2; j += 64) s3 += ex2((an + bsrc[j]) - s * row[j]);
+            rowerr += fabsf(wave_sum(s3) - mui);
+        }
+        if (lane == 0) ab[i] = an;
+    }
+    const float lw = STATS ? wave_sum(losspart) : 0.f;
+    if (lane == 0) {
+        scal[w] = rowerr;
+        scal[kWideRowWaves + w] = lw;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float re = 0.f, lo = 0.f;
+#pragma unroll
+        for (int q = 0; q < kWideRowWaves; ++q) {
+            re += scal[q];
+            lo += scal[kWideRowWaves + q];
+        }
+        const int plane = STATS ? 2 : (k & 1);
+        T.rowerr[((size_t)plane * T.R + r) * T.B + b] = re;
+        if (STATS) T.lossp[(size_t)r * T.B + b] = lo;
+    }
+}
+
+// Column partials over row block r of the plan (a, b) (after the rows pass's
+// u-update; STATS: the returned iterate), one thread per column; the entries
+// past d2 are written 0.  Four rows per step in separate accumulators, summed
+// in a fixed order.
+template <bool STATS>
+__global__ __launch_bounds__(kThreads) void sk_wide_cols(TiledArgs T, int k) {
+    const int j = blockIdx.x * kThreads + threadIdx.x;
+    const int r = blockIdx.y, b = blockIdx.z;
+    const int st = T.state[b];
+    if (!STATS && st != 0) return;  // block-uniform
+    const int K = STATS ? (st ? st : T.n_iter) : k;
+    const int d1 = T.d1, d2 = T.d2;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    if (j < d2) {
+        const float s = T.s;
+        const float bj = T.bbuf[(size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p + j];
+        const float *col = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0) + j;
+        const float *ab = T.a + (size_t)b * d1;
+        int i = i0;
+        for (; i + 4 <= i1; i += 4) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[q] += ex2((ab[i + q] + bj) - s * col[(size_t)(i + q) * d2]);
+        }
+        for (; i < i1; ++i) acc[0] += ex2((ab[i] + bj) - s * col[(size_t)i * d2]);
+    }
+    T.part[pidx(T, 0, r, b, j)] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
 // Mean point of each problem's two clouds (fixed-order sums): the centre of
 // the expansion form above.  One work-group per problem.
 __global__ __launch_bounds__(kThreads) void sk_tiled_center(TiledArgs T) {
@@ -1308,6 +1425,12 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
 // Cost kinds of the tiled regime: a shared cost, a per-sample cost, per-sample
 // point clouds (cost computed on the fly).
 constexpr int kKindShared = 0, kKindBatched = 1, kKindPoints = 2;
+// Rows wider than one wavefront's registers hold (d2 > kTiledMaxD2), shared
+// or per-sample cost: two passes per iteration (sk_wide_rows, sk_wide_cols).
+constexpr int kKindWide = 3;
+int tiled_kind(int d2, int c_batched) {
+    return d2 > kTiledMaxD2 ? kKindWide : (c_batched ? kKindBatched : kKindShared);
+}
 
 // Which sweep serves a problem: the shared-cost sweep with W problems per
 // work-group when C is shared and the batch fills at least four wavefronts,
@@ -1342,6 +1465,12 @@ void row_blocks(int B, int d1, int d2, int kind, int *R, int *RBS) {
         want = (target + G - 1) / G;
         want = (want + 7) / 8 * 8;
         unit = 1;
+    } else if (kind == kKindWide) {
+        // Wide rows: ~512 row blocks over the batch, at most 64 per problem
+        // (the merge reads R d2 partials per problem with one work-group).
+        want = (512 + B - 1) / (B > 0 ? B : 1);
+        want = want > 64 ? 64 : want;
+        unit = kWaves;
     } else {
         want = (2048 / kWaves + B - 1) / (B > 0 ? B : 1);
         unit = kWaves;
@@ -1379,6 +1508,7 @@ bool stream_shape(int d2, int kind) { return kind == kKindBatched && d2 % 4 == 0
 int stream_nc4(int d2) { return (d2 + 255) / 256; }
 int stream_waves(int d2) { return stream_nc4(d2) <= 8 ? 4 : 2; }
 int padded_width(int d2, int kind) {
+    if (kind == kKindWide) return (d2 + 255) / 256 * 256;  // the column pass's work-group width
     int w = 64 * ncw_bucket(d2);
     if (stream_shape(d2, kind)) w = w > 256 * nc4_bucket(d2) ? w : 256 * nc4_bucket(d2);
     return w;
@@ -1424,6 +1554,27 @@ hipError_t allow_lds(Kernel *kernel, size_t bytes) {
 
 // Launch sequence: init, exact first v-update (+ merge), n sweeps with a merge
 // after each but the last, stats sweep, final.
+// Launch sequence of the wide rows: as run_sequence, each sweep being a rows
+// pass and a columns pass.
+hipError_t run_wide(const TiledArgs &T, hipStream_t st) {
+    const dim3 blk(kThreads), rblk(64 * kWideRowWaves);
+    const dim3 rg(T.R, T.B), cg(T.d2p / kThreads, T.R, T.B);
+    hipLaunchKernelGGL(sk_tiled_init, dim3(512), blk, 0, st, T);
+    if (T.n_iter > 0) {
+        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+        hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), dim3(kMergeThreads), 0, st, T);
+        for (int k = 1; k <= T.n_iter; ++k) {
+            hipLaunchKernelGGL(sk_wide_rows<false>, rg, rblk, 0, st, T, k);
+            hipLaunchKernelGGL(sk_wide_cols<false>, cg, blk, 0, st, T, k);
+            if (k < T.n_iter) hipLaunchKernelGGL(sk_tiled_merge_cols<1024>, dim3(T.B), dim3(1024), 0, st, T, k);
+        }
+    }
+    hipLaunchKernelGGL(sk_wide_rows<true>, rg, rblk, 0, st, T, 0);
+    hipLaunchKernelGGL(sk_wide_cols<true>, cg, blk, 0, st, T, 0);
+    hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), blk, 0, st, T);
+    return hipGetLastError();
+}
+
 template <class Sweep, class Stats>
 hipError_t run_sequence(const TiledArgs &T, hipStream_t st, Sweep sweep, Stats stats) {
     const dim3 blk(kThreads);
@@ -1544,26 +1695,34 @@ hipError_t dispatch_shared(const TiledArgs &T, int ncw, hipStream_t st) {
     return run_shared<64, W, VEC4>(T, st);
 }
 
+// The row blocks of every chunk of a batch of B problems fit a grid dimension.
+bool row_blocks_fit(int B, int d1, int d2, int kind) {
+    int R, RBS;
+    row_blocks(tiled_chunk(B), d1, d2, kind, &R, &RBS);
+    if (R > 65535) return false;
+    if (B > kTiledMaxBatch && B % kTiledMaxBatch) {
+        row_blocks(B % kTiledMaxBatch, d1, d2, kind, &R, &RBS);
+        if (R > 65535) return false;
+    }
+    return true;
+}
+
 }  // namespace
 
 size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched) {
-    return layout(B, d1, d2, c_batched ? kKindBatched : kKindShared, nullptr, nullptr, nullptr).total;
+    return layout(tiled_chunk(B), d1, d2, tiled_kind(d2, c_batched), nullptr, nullptr, nullptr).total;
 }
 
 bool tiled_fits(int B, int d1, int d2, int c_batched) {
-    int R, RBS;
-    row_blocks(B, d1, d2, c_batched ? kKindBatched : kKindShared, &R, &RBS);
-    return d2 <= kTiledMaxD2 && B <= 65535 && R <= 65535;
+    return row_blocks_fit(B, d1, d2, tiled_kind(d2, c_batched));
 }
 
 bool tiled_points_fits(int B, int d1, int d2, int D) {
-    int R, RBS;
-    row_blocks(B, d1, d2, kKindPoints, &R, &RBS);
-    return D >= 1 && D <= kPointsMaxD && d2 <= kPointsMaxD2 && B <= 65535 && R <= 65535;
+    return D >= 1 && D <= kPointsMaxD && d2 <= kPointsMaxD2 && row_blocks_fit(B, d1, d2, kKindPoints);
 }
 
 size_t tiled_points_workspace_bytes(int B, int d1, int d2) {
-    return layout(B, d1, d2, kKindPoints, nullptr, nullptr, nullptr).total;
+    return layout(tiled_chunk(B), d1, d2, kKindPoints, nullptr, nullptr, nullptr).total;
 }
 
 namespace {
@@ -1605,15 +1764,17 @@ TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     T.RBS = RBS;
     T.JC = JC;
     T.n_iter = a.n_iter;
-    T.c_batched = kind != kKindShared;
+    T.c_batched = kind == kKindWide ? a.c_batched : kind != kKindShared;
     T.s = a.s;
     T.tol = a.tol;
     return T;
 }
 }  // namespace
 
-hipError_t launch_tiled_points(const FwdArgs &a, const float *X, const float *Y, int D, double rs, void *ws,
-                               hipStream_t st) {
+namespace {
+// One chunk (at most kTiledMaxBatch problems) of the points forward.
+hipError_t launch_tiled_points_chunk(const FwdArgs &a, const float *X, const float *Y, int D, double rs, void *ws,
+                                     hipStream_t st) {
     Layout L;
     TiledArgs T = tiled_args(a, kKindPoints, ws, &L);
     T.C = nullptr;
@@ -1630,9 +1791,12 @@ hipError_t launch_tiled_points(const FwdArgs &a, const float *X, const float *Y,
     }
 }
 
-hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
+// One chunk (at most kTiledMaxBatch problems) of the forward.
+hipError_t launch_tiled_chunk(const FwdArgs &a, void *ws, hipStream_t st) {
     Layout L;
-    TiledArgs T = tiled_args(a, a.c_batched ? kKindBatched : kKindShared, ws, &L);
+    const int kind = tiled_kind(a.d2, a.c_batched);
+    TiledArgs T = tiled_args(a, kind, ws, &L);
+    if (kind == kKindWide) return run_wide(T, st);
     char *base = static_cast<char *>(ws);
     const int ncw = (a.d2 + 63) / 64;
     const int W = shared_width(a.B, a.c_batched);
@@ -1669,6 +1833,20 @@ hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     }
     if (a.c_batched) return dispatch<true>(T, ncw, st);
     return dispatch<false>(T, ncw, st);
+}
+}  // namespace
+
+hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
+    return for_each_chunk(a.B, [&](int off, int n) { return launch_tiled_chunk(fwd_chunk(a, off, n), ws, st); });
+}
+
+// Per-sample clouds only (the on-the-fly sweep takes no shared clouds).
+hipError_t launch_tiled_points(const FwdArgs &a, const float *X, const float *Y, int D, double rs, void *ws,
+                               hipStream_t st) {
+    return for_each_chunk(a.B, [&](int off, int n) {
+        return launch_tiled_points_chunk(fwd_chunk(a, off, n), X + (size_t)off * a.d1 * D,
+                                         Y + (size_t)off * a.d2 * D, D, rs, ws, st);
+    });
 }
 
 }  // namespace sk

@@ -75,9 +75,20 @@ def test_regime_and_workspace_queries():
     assert sk.sinkhorn_regime(4, 10, 10, 0, lam=0.0) == 0
     assert sk.sinkhorn_workspace_bytes(4, 10, 10, 0, 0.1, 100) == 0
     assert sk.sinkhorn_workspace_bytes(256, 784, 784, 0, 0.01, 300) > 0
-    assert sk.sinkhorn_regime(4, 200, 4097, 0) == 0  # no kernel takes d2 > 4096 beyond the resident sizes
-    assert sk.sinkhorn_regime(65535, 130, 130, 0) == 2  # the tiled regime's largest batch
-    assert sk.sinkhorn_regime(65536, 130, 130, 0) == 0
+    # rows wider than 4096 take the two-pass sweep of the tiled regime
+    assert sk.sinkhorn_regime(4, 200, 4097, 0) == 2
+    assert sk.sinkhorn_regime(4, 3, 100000, 1) == 2
+    assert sk.sinkhorn_workspace_bytes(4, 200, 4097, 0, 0.1, 10) >= 4 * 4 * 4352  # column potentials, padded
+    # the tiled regime runs a batch above one grid dimension (65535) in chunks
+    # that share the workspace of one chunk
+    assert sk.sinkhorn_regime(65536, 130, 130, 0) == 2
+    assert sk.sinkhorn_regime(1 << 20, 130, 8, 1) == 2
+    chunk = sk.sinkhorn_workspace_bytes(65535, 130, 130, 0, 0.1, 10)
+    assert sk.sinkhorn_workspace_bytes(65536, 130, 130, 0, 0.1, 10) == chunk
+    assert sk.sinkhorn_workspace_bytes(200000, 130, 130, 0, 0.1, 10) == chunk
+    assert sk.sinkhorn_sharp_workspace_bytes(200000, 130, 8, 0) == sk.sinkhorn_sharp_workspace_bytes(65535, 130, 8, 0)
+    assert (sk.sinkhorn_points_workspace_bytes(70000, 130, 8, 1, 3, 0.1, 10)
+            == sk.sinkhorn_points_workspace_bytes(65535, 130, 8, 1, 3, 0.1, 10))
     assert sk.sinkhorn_regime(1 << 20, 8, 8, 0) == 1  # the resident regime has no such limit
     assert sk.sinkhorn_workspace_bytes(-1, 784, 784, 0, 0.01, 300) == 0
 

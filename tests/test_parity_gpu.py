@@ -708,6 +708,47 @@ def test_tiled_on_side_stream():
     check_forward(prob, gpu=gpu)
 
 
+@pytest.mark.parametrize("c_batched,tol", [(False, 0.0), (True, 2e-4)])
+def test_tiled_batch_above_grid_limit(c_batched, tol):
+    """65537 problems of a tiled shape: more than one grid dimension holds,
+    so the batch runs as two chunks (65535 + 2) that share one workspace.
+    Problems on both sides of the boundary against the oracle, forward and
+    backward, with a shared cost and with per-sample costs and early stop."""
+    prob = workloads.random_problem(seed=91, B=65537, d1=130, d2=8, lam=0.1, n_iter=40, c_batched=c_batched,
+                                    tol=tol)
+    assert sk.sinkhorn_regime(prob.B, prob.d1, prob.d2, int(c_batched)) == 2
+    idx = np.array([0, 1, 65533, 65534, 65535, 65536])
+    gpu, ref = check_forward(prob, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx, grad_C=c_batched)
+
+
+@pytest.mark.parametrize("B,d1,d2,c_batched,lam,n_iter,zero_frac,tol", [
+    (5, 150, 5000, False, 0.1, 30, 0.0, 0.0),    # shared cost, rows just past one wavefront's registers
+    (3, 9, 6000, True, 0.05, 40, 0.2, 1e-3),     # per-sample costs, zero masses, early stop, few rows
+    (2, 300, 4097, False, 0.005, 40, 0.0, 0.0),  # ragged width, small lambda (exact fallbacks)
+    (4, 130, 9000, True, 0.02, 25, 0.1, 0.0),
+    (2, 3, 100000, True, 0.1, 20, 0.0, 0.0),     # 100000 columns, 3 rows
+])
+def test_wide_rows(B, d1, d2, c_batched, lam, n_iter, zero_frac, tol):
+    """Rows wider than one wavefront's registers hold (d2 > 4096): two passes
+    over the cost per iteration; forward and backward (with grad_C) against
+    the oracle on every problem."""
+    prob = workloads.random_problem(seed=d2 + d1, B=B, d1=d1, d2=d2, lam=lam, n_iter=n_iter, c_batched=c_batched,
+                                    zero_frac=zero_frac, tol=tol)
+    assert sk.sinkhorn_regime(B, d1, d2, int(c_batched)) == 2
+    gpu, ref = check_forward(prob)
+    check_backward(prob, gpu, ref, grad_C=True)
+
+
+def test_wide_grid_image_sampled():
+    """Image histograms on a 91x91 grid (d = 8281, shared squared grid cost of
+    274 MB, lambda 0.01), B = 8: the first and last problems against the oracle."""
+    prob = workloads.image(B=8, side=91, n_iter=100, lam=0.01)
+    idx = np.array([0, 7])
+    gpu, ref = check_forward(prob, idx=idx)
+    check_backward(prob, gpu, ref, idx=idx)
+
+
 def test_shared_grad_C_many_rows():
     """A shared cost with d1 = 70000 rows (more than a grid's y dimension):
     the forward runs in the tiled regime and grad_C (rows grid-strided) covers

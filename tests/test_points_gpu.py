@@ -178,3 +178,11 @@ def test_points_invalid_dimension():
     prob = workloads.random_points(57, B=2, d1=10, d2=12, D=17, lam=0.1, n_iter=5)
     with pytest.raises(sk.SinkhornError):
         _gpu(prob)
+
+
+def test_points_batch_above_grid_limit():
+    """65537 per-sample clouds of a tiled shape through the on-the-fly sweep,
+    run as two chunks of the batch: problems on both sides of the boundary
+    against the oracle, with the point gradients."""
+    prob = workloads.random_points(seed=93, B=65537, d1=130, d2=8, D=3, lam=0.2, n_iter=30)
+    check_points(prob, idx=np.array([0, 65534, 65535, 65536]))

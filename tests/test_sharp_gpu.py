@@ -159,6 +159,13 @@ def test_sharp_tiled_iteration_cap_and_deterministic():
         np.testing.assert_array_equal(a[k].cpu().numpy(), b[k].cpu().numpy())
 
 
+def test_sharp_tiled_batch_above_grid_limit():
+    """The tiled sharp gradient on 65537 problems (two chunks of the batch):
+    problems on both sides of the boundary against the dense solve."""
+    prob = workloads.random_problem(seed=95, B=65537, d1=130, d2=8, lam=0.2, n_iter=200)
+    check_sharp(prob, idx=np.array([0, 65534, 65535, 65536]), max_cg=400)
+
+
 def test_sharp_autograd_wrapper():
     prob = workloads.random_problem(seed=44, B=4, d1=24, d2=30, lam=0.1, n_iter=300)
     mu = _t(prob.mu).requires_grad_()
