@@ -928,6 +928,12 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
         __syncthreads();                     // ... and every other wavefront's
         if (ch + 1 < nchunk) issue_chunk(ch + 1);
         const float *cbuf = lds + (ch & 1) * RS * D2P + lane;
+        // One row per batch (the widest rows): the next row's first 4 staged
+        // values are read before this row's reduction, so their latency is
+        // hidden instead of exposed at the next row's start (1.8 % on 4096
+        // columns).  Narrower rows gain too little to pay its registers.
+        constexpr int PF = 4;
+        float pre[PF];
 #pragma unroll
         for (int rb = 0; rb < RS; rb += RB) {
             const int rel = ch * RS + rb;
@@ -966,7 +972,14 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                     for (int n = g * G; n < (g + 1) * G && n < NE; ++n)
                         e[n / NCW][n % NCW] = cbuf[rq[n / NCW] * D2P + 64 * (n % NCW)];
                 };
-                read_group(0);
+                if (RB == 1 && rb > 0) {  // group 0 of the batch is row rb's first G values
+#pragma unroll
+                    for (int n = 0; n < PF; ++n) e[0][n] = pre[n];
+#pragma unroll
+                    for (int n = PF; n < G; ++n) e[0][n] = cbuf[rb * D2P + 64 * n];
+                } else {
+                    read_group(0);
+                }
                 __builtin_amdgcn_sched_barrier(0);
                 // The exponentials at the lowest issue priority, the batch's
                 // serial reduction and update at the highest, so that another
@@ -981,6 +994,10 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                         e[q][c] = ex2(__builtin_fmaf(e[q][c], ns, ai[q] + bv[c]));
                     }
                     __builtin_amdgcn_sched_barrier(0);
+                }
+                if (RB == 1 && rb + 1 < RS) {  // the next row of this chunk (staged; unused if past the block)
+#pragma unroll
+                    for (int n = 0; n < PF; ++n) pre[n] = cbuf[(rb + 1) * D2P + 64 * n];
                 }
 #pragma unroll
                 for (int q = 0; q < RB; ++q) p[q] = tree_sum<NCW>(e[q]);
