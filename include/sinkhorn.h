@@ -49,10 +49,8 @@ extern "C" {
 typedef enum {
     SK_OK = 0,
     SK_ERR_NULLPTR = -1,   /* a required pointer is NULL                     */
-    SK_ERR_SHAPE = -2,     /* B < 0, d1 < 1, d2 < 1, d1 or d2 > 2^24, sizes
-                              overflow (d1 d2 > 2^40, B d1 d2 > 2^46), or
-                              (sinkhorn_backward_sharp only) d2 > 4096 with
-                              max(d1, d2) > 128                             */
+    SK_ERR_SHAPE = -2,     /* B < 0, d1 < 1, d2 < 1, d1 or d2 > 2^24, or
+                              sizes overflow (d1 d2 > 2^40, B d1 d2 > 2^46) */
     SK_ERR_LAMBDA = -3,    /* lambda not finite and > 0                       */
     SK_ERR_ITERS = -4,     /* n_iter < 0, or tol not finite                   */
     SK_ERR_WORKSPACE = -5, /* ws_bytes < sinkhorn_workspace_bytes(p)          */

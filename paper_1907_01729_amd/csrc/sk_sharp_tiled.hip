@@ -140,6 +140,81 @@ __global__ __launch_bounds__(kShtThreads) void sk_sht_sweep(ShtArgs T) {
     }
 }
 
+// Rows wider than one wavefront's registers hold (d2 > kTiledMaxD2): each
+// product takes two passes over the cells, one exponential per cell in each.
+// The rows pass (one wavefront per row, looping over the columns) forms the
+// row half (SETUP: the plan's row marginal and (P o C) 1); the columns pass
+// (one thread per column, looping over a row block) the row blocks' column
+// partials.  Setup, update and final are those of the one-pass sweep.
+constexpr int kShtWideWaves = 16;
+
+template <bool SETUP>
+__global__ __launch_bounds__(64 * kShtWideWaves) void sk_sht_rows(ShtArgs T) {
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (!SETUP && T.sc[(size_t)b * 4 + 3] != 0.f) return;  // work-group-uniform
+    const int d1 = T.d1, d2 = T.d2;
+    const float *Cb = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0);
+    const float *bv = T.b2 + (size_t)b * T.d2p;
+    const float *pg = T.pg + (size_t)b * T.d2p;
+    const float ns = -T.s;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    for (int i = i0 + w; i < i1; i += kShtWideWaves) {
+        const float ai = T.a2[(size_t)b * d1 + i];
+        const float *crow = Cb + (size_t)i * d2;
+        float x0 = 0.f, x1 = 0.f;
+        for (int j = lane; j < d2; j += 64) {
+            const float cij = crow[j];
+            const float e = ex2((ai + bv[j]) + ns * cij);
+            if (SETUP) {
+                x0 += e;
+                x1 = __builtin_fmaf(e, cij, x1);
+            } else {
+                x0 = __builtin_fmaf(e, pg[j], x0);
+            }
+        }
+        x0 = wave_sum(x0);
+        if (SETUP) x1 = wave_sum(x1);
+        if (lane == 0) {
+            if (SETUP) {
+                T.dgf[(size_t)b * d1 + i] = x0;
+                T.rf[(size_t)b * d1 + i] = x1;
+            } else {
+                T.Pp[(size_t)b * d1 + i] = x0;
+            }
+        }
+    }
+}
+
+template <bool SETUP>
+__global__ __launch_bounds__(kShtThreads) void sk_sht_cols(ShtArgs T) {
+    const int j = blockIdx.x * kShtThreads + threadIdx.x;
+    const int r = blockIdx.y, b = blockIdx.z;
+    if (!SETUP && T.sc[(size_t)b * 4 + 3] != 0.f) return;  // work-group-uniform
+    const int d1 = T.d1, d2 = T.d2;
+    const int i0 = r * T.RBS, i1 = min(d1, i0 + T.RBS);
+    float c0 = 0.f, c1 = 0.f;
+    if (j < d2) {
+        const float bj = T.b2[(size_t)b * T.d2p + j];
+        const float *col = T.C + (T.c_batched ? (size_t)b * d1 * d2 : 0) + j;
+        const float *ab = T.a2 + (size_t)b * d1;
+        const float *pf = T.pf + (size_t)b * d1;
+        const float ns = -T.s;
+        for (int i = i0; i < i1; ++i) {
+            const float cij = col[(size_t)i * d2];
+            const float e = ex2((ab[i] + bj) + ns * cij);
+            if (SETUP) {
+                c0 += e;
+                c1 = __builtin_fmaf(e, cij, c1);
+            } else {
+                c0 = __builtin_fmaf(e, pf[i], c0);
+            }
+        }
+    }
+    T.part[ppart(T, 0, r, b, j)] = c0;
+    if (SETUP) T.part[ppart(T, 1, r, b, j)] = c1;
+}
+
 // Fixed-order sum over the row blocks of column j's partial in plane pl.
 __device__ __forceinline__ float merge_col(const ShtArgs &T, int pl, int b, int j) {
     float v = 0.f;
@@ -318,8 +393,11 @@ int sht_ncw(int d2) {
 
 // Row blocks: about 512 work-groups in all, rows per block a multiple of the
 // wavefronts per work-group.
-void sht_row_blocks(int B, int d1, int *R, int *RBS) {
+void sht_row_blocks(int B, int d1, int d2, int *R, int *RBS) {
     int want = (512 + B - 1) / (B > 0 ? B : 1);
+    // Wide rows: at most 64 row blocks (the update merges R d2 partials per
+    // problem with one work-group).
+    if (d2 > kTiledMaxD2 && want > 64) want = 64;
     const int maxR = (d1 + kShtWaves - 1) / kShtWaves;
     want = want < 1 ? 1 : (want > maxR ? maxR : want);
     int rbs = (d1 + want - 1) / want;
@@ -335,8 +413,8 @@ struct ShtLayout {
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
 ShtLayout sht_layout(int B, int d1, int d2, int *R, int *RBS, int *d2p) {
-    sht_row_blocks(B, d1, R, RBS);
-    *d2p = 64 * sht_ncw(d2);
+    sht_row_blocks(B, d1, d2, R, RBS);
+    *d2p = d2 > kTiledMaxD2 ? (d2 + kShtThreads - 1) / kShtThreads * kShtThreads : 64 * sht_ncw(d2);
     const size_t f1 = sizeof(float) * (size_t)B * d1, f2 = sizeof(float) * (size_t)B * *d2p;
     ShtLayout L;
     size_t off = 0;
@@ -368,6 +446,21 @@ ShtLayout sht_layout(int B, int d1, int d2, int *R, int *RBS, int *d2p) {
     off = al256(off + sizeof(float) * 4 * (size_t)B);
     L.total = off;
     return L;
+}
+
+hipError_t run_sht_wide(const ShtArgs &T, hipStream_t st) {
+    const dim3 rg(T.R, T.B), rblk(64 * kShtWideWaves), cg(T.d2p / kShtThreads, T.R, T.B), cblk(kShtThreads);
+    hipLaunchKernelGGL(sk_sht_prep, dim3(T.B), dim3(kShuThreads), 0, st, T);
+    hipLaunchKernelGGL(sk_sht_rows<true>, rg, rblk, 0, st, T);
+    hipLaunchKernelGGL(sk_sht_cols<true>, cg, cblk, 0, st, T);
+    hipLaunchKernelGGL(sk_sht_setup, dim3(T.B), dim3(kShuThreads), 0, st, T);
+    for (int it = 0; it < T.max_cg; ++it) {
+        hipLaunchKernelGGL(sk_sht_rows<false>, rg, rblk, 0, st, T);
+        hipLaunchKernelGGL(sk_sht_cols<false>, cg, cblk, 0, st, T);
+        hipLaunchKernelGGL(sk_sht_update, dim3(T.B), dim3(kShuThreads), 0, st, T);
+    }
+    hipLaunchKernelGGL(sk_sht_final, dim3(T.B), dim3(kShuThreads), 0, st, T);
+    return hipGetLastError();
 }
 
 template <int NCW>
@@ -423,6 +516,7 @@ hipError_t launch_sharp_tiled_chunk(const SharpArgs &a, void *ws, hipStream_t st
     T.max_cg = a.max_cg;
     T.s = a.s;
     T.cg_tol = a.cg_tol;
+    if (a.d2 > kTiledMaxD2) return run_sht_wide(T, st);
     switch (sht_ncw(a.d2)) {
         case 4: return run_sht<4>(T, st);
         case 8: return run_sht<8>(T, st);
@@ -442,13 +536,13 @@ size_t sharp_tiled_workspace_bytes(int B, int d1, int d2) {
 
 bool sharp_tiled_fits(int B, int d1, int d2) {
     int R, RBS;
-    sht_row_blocks(tiled_chunk(B), d1, &R, &RBS);
+    sht_row_blocks(tiled_chunk(B), d1, d2, &R, &RBS);
     if (R > 65535) return false;
     if (B > kTiledMaxBatch && B % kTiledMaxBatch) {
-        sht_row_blocks(B % kTiledMaxBatch, d1, &R, &RBS);
+        sht_row_blocks(B % kTiledMaxBatch, d1, d2, &R, &RBS);
         if (R > 65535) return false;
     }
-    return d2 <= kTiledMaxD2;
+    return true;
 }
 
 hipError_t launch_sharp_tiled(const SharpArgs &a, void *ws, hipStream_t st) {

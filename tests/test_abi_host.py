@@ -189,7 +189,12 @@ def test_sharp_rejections_on_host():
         a = ctypes.c_void_p(ptr) if ptr else None
         return lib.sinkhorn_backward_sharp(ctypes.byref(p), a, a, a, a, a, a, a, a, max_cg, ctypes.c_float(tol),
                                            None, a, ctypes.c_size_t(ws), None)
-    assert call(_binding.problem(4, 200, 4097, 0, 0.1, 0)) == -2  # no kernel takes d2 > 4096 beyond 128
+    # rows wider than 4096 take the two-pass products: a workspace, then pointers
+    wide = sk.sinkhorn_sharp_workspace_bytes(4, 200, 4097, 0)
+    assert wide > 0
+    assert call(_binding.problem(4, 200, 4097, 0, 0.1, 0), ws=wide - 1, ptr=0x1000) == -5
+    assert call(_binding.problem(4, 200, 4097, 0, 0.1, 0), ws=wide) == -1
+    assert call(_binding.problem(4, 0, 4097, 0, 0.1, 0)) == -2
     assert call(_binding.problem(4, 10, 10, 0, 0.0, 0)) == -3
     assert call(_binding.problem(4, 10, 10, 0, 0.1, 0), max_cg=0) == -4
     assert call(_binding.problem(4, 10, 10, 0, 0.1, 0), tol=float("nan")) == -4
@@ -200,6 +205,6 @@ def test_sharp_rejections_on_host():
     need = sk.sinkhorn_sharp_workspace_bytes(4, 129, 10, 0)
     assert need > 0
     assert sk.sinkhorn_sharp_workspace_bytes(256, 784, 784, 0) > 0
-    assert sk.sinkhorn_sharp_workspace_bytes(4, 200, 4097, 0) == 0  # invalid problem
+    assert sk.sinkhorn_sharp_workspace_bytes(4, 0, 4097, 0) == 0  # invalid problem
     assert call(_binding.problem(4, 129, 10, 0, 0.1, 0), ws=need - 1, ptr=0x1000) == -5
     assert call(_binding.problem(4, 129, 10, 0, 0.1, 0), ws=need) == -1  # then the pointers are checked

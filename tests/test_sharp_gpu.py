@@ -166,6 +166,15 @@ def test_sharp_tiled_batch_above_grid_limit():
     check_sharp(prob, idx=np.array([0, 65534, 65535, 65536]), max_cg=400)
 
 
+@pytest.mark.parametrize("d1,d2,c_batched,zero_frac", [(140, 4100, False, 0.0), (5, 4500, True, 0.2)])
+def test_sharp_tiled_wide_rows(d1, d2, c_batched, zero_frac):
+    """Rows wider than 4096 columns: every product in two passes over the
+    cost (rows, then columns); against the dense solve."""
+    prob = workloads.random_problem(seed=97 + d2, B=2, d1=d1, d2=d2, lam=0.3, n_iter=150, c_batched=c_batched,
+                                    zero_frac=zero_frac)
+    check_sharp(prob, max_cg=1000)
+
+
 def test_sharp_autograd_wrapper():
     prob = workloads.random_problem(seed=44, B=4, d1=24, d2=30, lam=0.1, n_iter=300)
     mu = _t(prob.mu).requires_grad_()
