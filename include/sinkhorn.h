@@ -148,6 +148,20 @@ SK_API sk_status sinkhorn_forward_select(const sk_problem *p, int32_t select, co
                                          size_t ws_bytes, void *stream);
 
 /*
+ * Dispatch report, for logging and debugging (nothing is launched): writes
+ * into buf a one-line, NUL-terminated description of the kernels and launch
+ * shape that sinkhorn_forward_select(p, select, ...) takes for *p: the
+ * regime, the kernel instantiations, row blocks, merges, hand-overs and the
+ * workspace size.  snprintf semantics: at most len bytes are written (buf may
+ * be NULL when len is 0) and the return value is the length of the whole
+ * line without the NUL.  Invalid problem: its (negative) status; unknown
+ * selector: SK_ERR_ARG.  The symmetry of a shared cost is only tested on the
+ * device, so the report names the symmetric kernel with its in-place general
+ * iteration.
+ */
+SK_API int32_t sinkhorn_describe(const sk_problem *p, int32_t select, char *buf, size_t len);
+
+/*
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the forward
  * of sinkhorn_forward without a workspace argument.  Its scratch is a fixed

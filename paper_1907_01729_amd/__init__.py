@@ -23,6 +23,7 @@ from ._binding import (  # noqa: F401
     sinkhorn_forward_select,
     sinkhorn_points_workspace_bytes,
     sinkhorn_regime,
+    sinkhorn_describe,
     sinkhorn_sharp_workspace_bytes,
     sinkhorn_status_string,
     sinkhorn_workspace_bytes,
@@ -47,6 +48,7 @@ __all__ = [
     "sinkhorn_loss_points",
     "sinkhorn_points_workspace_bytes",
     "sinkhorn_regime",
+    "sinkhorn_describe",
     "sinkhorn_sharp_workspace_bytes",
     "sinkhorn_status_string",
     "sinkhorn_workspace_bytes",

@@ -38,6 +38,7 @@ EXPORTED = (
     "sinkhorn_backward_points",
     "sinkhorn_backward_sharp",
     "sinkhorn_sharp_workspace_bytes",
+    "sinkhorn_describe",
 )
 
 
@@ -100,6 +101,8 @@ def load_library():
     lib.sinkhorn_backward_sharp.restype = ctypes.c_int
     lib.sinkhorn_sharp_workspace_bytes.argtypes = [PP]
     lib.sinkhorn_sharp_workspace_bytes.restype = ctypes.c_size_t
+    lib.sinkhorn_describe.argtypes = [PP, I, ctypes.c_char_p, ctypes.c_size_t]
+    lib.sinkhorn_describe.restype = ctypes.c_int32
     _lib = lib
     return lib
 
@@ -120,6 +123,21 @@ def sinkhorn_workspace_bytes(B, d1, d2, c_batched, lam, n_iter, tol=0.0) -> int:
 def sinkhorn_regime(B, d1, d2, c_batched, lam=1.0, n_iter=1, tol=0.0) -> int:
     p = problem(B, d1, d2, c_batched, lam, n_iter, tol)
     return int(load_library().sinkhorn_regime(ctypes.byref(p)))
+
+
+def sinkhorn_describe(B, d1, d2, c_batched=0, lam=1.0, n_iter=1, tol=0.0, select="default") -> str:
+    """The kernels and launch shape a forward takes for this problem (one line;
+    nothing is launched).  Raises SinkhornError for an invalid problem."""
+    if select not in SK_SELECT:
+        raise ValueError(f"select must be one of {sorted(SK_SELECT)}, got {select!r}")
+    lib = load_library()
+    p = problem(B, d1, d2, c_batched, lam, n_iter, tol)
+    n = int(lib.sinkhorn_describe(ctypes.byref(p), SK_SELECT[select], None, 0))
+    if n < 0:
+        raise SinkhornError(n, "sinkhorn_describe")
+    buf = ctypes.create_string_buffer(n + 1)
+    lib.sinkhorn_describe(ctypes.byref(p), SK_SELECT[select], buf, n + 1)
+    return buf.value.decode()
 
 
 def _dev(t: torch.Tensor, name: str, dtype=torch.float32) -> torch.Tensor:

@@ -2,6 +2,7 @@
 // regime dispatch and launches.  No allocation, no synchronisation.
 #include <math.h>
 #include <stdint.h>
+#include <stdio.h>
 
 #include <mutex>
 
@@ -86,6 +87,27 @@ sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, cons
     a.select = SK_SELECT_DEFAULT;
     a.only_marked = 0;
     return a;
+}
+
+// The resident regime's choice (launch_resident_regime) in one line.
+int resident_describe(const sk::FwdArgs &a, char *buf, size_t len) {
+    const int nb = ((a.d1 > a.d2 ? a.d1 : a.d2) + 7) / 8;
+    const int N = nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : nb <= 13 ? 13 : 16;
+    if (a.select == SK_SELECT_LOG_ONLY || a.n_iter <= 0)
+        return snprintf(buf, len,
+                        "resident: sk_resident_log_kernel<%d> (log domain, two wavefronts per problem, the scaled "
+                        "cost in registers, every iteration in one launch)",
+                        N);
+    const bool sym = a.select != SK_SELECT_NO_SYMMETRIC && !a.c_batched && a.d1 == a.d2 && N <= 13;
+    const char *hand = a.select == SK_SELECT_PLAIN_ONLY
+                           ? "a problem out of fp32 range is left unsolved (iters = -1)"
+                           : (N <= 13 ? "a problem out of fp32 range is re-solved in the log domain in place"
+                                      : "a problem out of fp32 range is re-solved by a second launch, "
+                                        "sk_resident_log_kernel<16>");
+    return snprintf(buf, len,
+                    "resident: %s<%d> (plain form, K in registers, two wavefronts per problem%s); %s",
+                    sym ? "sk_resident_sym_kernel" : "sk_resident_gen_kernel", N,
+                    sym ? "; the general iteration in place if the cost is not symmetric" : "", hand);
 }
 
 // Regime dispatch of a forward over a cost matrix (tiled sweep, or the
@@ -177,6 +199,18 @@ size_t sinkhorn_workspace_bytes(const sk_problem *p) {
     if (check_problem(p) != SK_OK) return 0;
     if (sk::resident_fits(p->d1, p->d2)) return 0;
     return sk::tiled_workspace_bytes(p->B, p->d1, p->d2, p->c_batched);
+}
+
+int32_t sinkhorn_describe(const sk_problem *p, int32_t select, char *buf, size_t len) {
+    if (select < SK_SELECT_DEFAULT || select > SK_SELECT_NO_COMPACTION) return SK_ERR_ARG;
+    const sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (!buf && len) return SK_ERR_NULLPTR;
+    sk::FwdArgs a = fwd_args(p, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    a.select = select;
+    if (p->B == 0) return snprintf(buf, len, "nothing to launch (B = 0)");
+    if (!sk::resident_fits(p->d1, p->d2)) return sk::tiled_describe(a, buf, len);
+    return resident_describe(a, buf, len);
 }
 
 sk_status sinkhorn_forward_select(const sk_problem *p, int32_t select, const float *mu, const float *nu,

@@ -88,6 +88,9 @@ hipError_t for_each_chunk(int B, Launch launch) {
 bool tiled_fits(int B, int d1, int d2, int c_batched);
 size_t tiled_workspace_bytes(int B, int d1, int d2, int c_batched);
 hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st);
+// One line on the kernels and launch shape launch_tiled takes for a (snprintf
+// semantics: the length of the whole line).
+int tiled_describe(const FwdArgs &a, char *buf, size_t len);
 
 hipError_t launch_backward(const BwdArgs &a, hipStream_t st);
 

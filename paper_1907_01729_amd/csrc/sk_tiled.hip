@@ -29,6 +29,8 @@
 // which every later sweep and merge honours.  In the streaming sweep every
 // work-group of b sums the same partials in the same order, so all take the
 // same decision, and the first row block records it.
+#include <stdio.h>
+
 #include "sk_device.h"
 #include "sk_internal.h"
 
@@ -1852,6 +1854,46 @@ hipError_t launch_tiled_chunk(const FwdArgs &a, void *ws, hipStream_t st) {
     return dispatch<false>(T, ncw, st);
 }
 }  // namespace
+
+int tiled_describe(const FwdArgs &a, char *buf, size_t len) {
+    const int B = tiled_chunk(a.B);
+    const int kind = tiled_kind(a.d2, a.c_batched);
+    int R, RBS, JC;
+    const Layout L = layout(B, a.d1, a.d2, kind, &R, &RBS, &JC);
+    const int W = shared_width(B, kind), ncw = ncw_bucket(a.d2);
+    char sweep[192];
+    bool merge = true;
+    if (kind == kKindWide) {
+        snprintf(sweep, sizeof sweep, "sk_wide_rows + sk_wide_cols (two passes over the cost per iteration)");
+    } else if (W) {
+        const int RB = ncw <= 16 ? 4 : (ncw <= 32 ? 2 : 1), RS = ncw <= 16 ? 8 : 4;
+        snprintf(sweep, sizeof sweep,
+                 "sk_tiled_sweep_shared<%d, %d, %d, %d> (%d problems per work-group, cost rows staged through LDS "
+                 "%d at a time)",
+                 ncw, W, RS, RB, W, RS);
+    } else if (stream_shape(a.d2, kind)) {
+        snprintf(sweep, sizeof sweep,
+                 "sk_tiled_sweep_stream<%d> (the cost streamed once per iteration; "
+                 "sk_tiled_sweep<%d> if its rows are not 16-byte aligned)",
+                 stream_nc4(a.d2), ncw);
+        merge = false;
+    } else {
+        snprintf(sweep, sizeof sweep, "sk_tiled_sweep<%d> (one problem per work-group)", ncw);
+    }
+    char mrg[128];
+    if (merge)
+        snprintf(mrg, sizeof mrg, "sk_tiled_merge_cols<%d> after each sweep (one work-group per problem)",
+                 kind == kKindWide || a.d2 > 1024 ? 1024 : 256);
+    else
+        snprintf(mrg, sizeof mrg, "the merge folded into the next sweep");
+    const bool compact = W && a.tol > 0.f && a.select != SK_SELECT_NO_COMPACTION;
+    const int nchunk = (a.B + kTiledMaxBatch - 1) / kTiledMaxBatch;
+    char chunks[64] = "";
+    if (nchunk > 1) snprintf(chunks, sizeof chunks, "; %d chunks of at most %d problems", nchunk, kTiledMaxBatch);
+    return snprintf(buf, len, "tiled: %s; %d row block%s of %d rows; %s%s%s; workspace %zu bytes", sweep, R,
+                    R == 1 ? "" : "s", RBS, mrg, compact ? "; the running list rebuilt after stops" : "", chunks,
+                    L.total);
+}
 
 hipError_t launch_tiled(const FwdArgs &a, void *ws, hipStream_t st) {
     return for_each_chunk(a.B, [&](int off, int n) { return launch_tiled_chunk(fwd_chunk(a, off, n), ws, st); });

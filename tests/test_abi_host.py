@@ -208,3 +208,41 @@ def test_sharp_rejections_on_host():
     assert sk.sinkhorn_sharp_workspace_bytes(4, 0, 4097, 0) == 0  # invalid problem
     assert call(_binding.problem(4, 129, 10, 0, 0.1, 0), ws=need - 1, ptr=0x1000) == -5
     assert call(_binding.problem(4, 129, 10, 0, 0.1, 0), ws=need) == -1  # then the pointers are checked
+
+
+def test_describe_names_the_dispatch():
+    d = sk.sinkhorn_describe
+    label = d(1024, 100, 100, 0, 0.05, 200)
+    assert label.startswith("resident: sk_resident_sym_kernel<13>") and "in place" in label
+    assert "sk_resident_log_kernel<13>" in d(1024, 100, 100, 0, 0.05, 200, select="log")
+    assert "sk_resident_gen_kernel<13>" in d(1024, 100, 100, 0, 0.05, 200, select="nosym")
+    assert "left unsolved" in d(1024, 100, 100, 0, 0.05, 200, select="plain")
+    wide_res = d(8, 120, 120, 1, 0.1, 10)
+    assert "sk_resident_gen_kernel<16>" in wide_res and "second launch" in wide_res
+    assert "sk_resident_log_kernel<2>" in d(4, 10, 10, 0, 0.1, 0)  # n_iter = 0
+    grid = d(64, 4096, 4096, 0, 1e-3, 500, 1e-6)
+    assert "sk_tiled_sweep_shared<64, 8, 4, 1>" in grid and "32 row blocks of 128 rows" in grid
+    assert "running list" in grid and "running list" not in d(64, 4096, 4096, 0, 1e-3, 500, 1e-6, select="nocompact")
+    assert f"workspace {sk.sinkhorn_workspace_bytes(64, 4096, 4096, 0, 1e-3, 500, 1e-6)} bytes" in grid
+    assert "sk_tiled_sweep_shared<13, 8, 8, 4>" in d(256, 784, 784, 0, 0.01, 300)
+    clouds = d(32, 1024, 2048, 1, 0.05, 100)
+    assert "sk_tiled_sweep_stream<8>" in clouds and "folded" in clouds
+    assert "sk_tiled_sweep<4>" in d(2, 300, 200, 0, 0.1, 10)  # a shared cost with B < 4
+    assert "sk_wide_rows" in d(4, 200, 5000, 0, 0.1, 10)
+    assert "2 chunks" in d(70000, 130, 8, 1, 0.1, 10)
+    assert d(0, 10, 10, 0, 0.1, 10).startswith("nothing")
+
+
+def test_describe_truncates_and_rejects():
+    lib = sk.load_library()
+    p = _binding.problem(64, 4096, 4096, 0, 1e-3, 500)
+    n = lib.sinkhorn_describe(ctypes.byref(p), 0, None, 0)
+    assert n > 40
+    buf = ctypes.create_string_buffer(b"x" * 32)
+    assert lib.sinkhorn_describe(ctypes.byref(p), 0, buf, 16) == n  # snprintf semantics
+    assert len(buf.value) == 15 and buf.raw[16:32] == b"x" * 16
+    assert lib.sinkhorn_describe(ctypes.byref(p), 9, None, 0) == -7
+    assert lib.sinkhorn_describe(ctypes.byref(_binding.problem(4, 0, 10, 0, 0.1, 10)), 0, None, 0) == -2
+    assert lib.sinkhorn_describe(ctypes.byref(p), 0, None, 8) == -1
+    with pytest.raises(_binding.SinkhornError):
+        sk.sinkhorn_describe(4, 10, 10, 0, lam=0.0)
