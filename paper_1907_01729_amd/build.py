@@ -7,6 +7,7 @@ from __future__ import annotations
 
 import glob
 import os
+import shlex
 import shutil
 import subprocess
 from concurrent.futures import ThreadPoolExecutor
@@ -46,20 +47,42 @@ def _run(cmd, verbose):
         print(r.stderr, flush=True)
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
-    os.makedirs(OBJ_DIR, exist_ok=True)
+def _compile_and_link(flags, obj_dir, lib, link_extra=(), verbose=False, jobs=None) -> str:
+    os.makedirs(obj_dir, exist_ok=True)
     cc = hipcc()
     srcs = sources()
-    objs = [os.path.join(OBJ_DIR, os.path.basename(s)[:-4] + ".o") for s in srcs]
+    objs = [os.path.join(obj_dir, os.path.basename(s)[:-4] + ".o") for s in srcs]
     jobs = jobs or min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
     with ThreadPoolExecutor(max_workers=jobs) as ex:
-        futs = [ex.submit(_run, [cc, *HIP_FLAGS, "-c", "-o", o, s], verbose) for s, o in zip(srcs, objs)]
+        futs = [ex.submit(_run, [cc, *flags, "-c", "-o", o, s], verbose) for s, o in zip(srcs, objs)]
         for f in futs:
             f.result()
-    tmp = LIB + ".tmp"
-    _run([cc, *HIP_FLAGS, "-shared", "-o", tmp, *objs], verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    tmp = lib + ".tmp"
+    _run([cc, *flags, "-shared", *link_extra, "-o", tmp, *objs], verbose)
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    return _compile_and_link(HIP_FLAGS, OBJ_DIR, LIB, verbose=verbose, jobs=jobs)
+
+
+# Host-side sanitizers for the CPU checks of the C ABI: AddressSanitizer and
+# UndefinedBehaviorSanitizer on the host pass only (device code as above),
+# the sanitizer runtime linked as a shared library.
+HOST_SANITIZE = shlex.split(
+    "-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined "
+    "-Xarch_host -fno-sanitize-recover=all -Xarch_host -fno-omit-frame-pointer")
+
+
+def build_host_sanitized(verbose: bool = False, jobs: int | None = None) -> str:
+    """A copy of the library with sanitized host code, in _build/asan (for
+    tests that call only host-side paths of the ABI; never loaded by the
+    package)."""
+    out = os.path.join(OBJ_DIR, "asan")
+    flags = [f if f != "-O3" else "-O1" for f in HIP_FLAGS] + ["-g"] + HOST_SANITIZE
+    return _compile_and_link(flags, out, os.path.join(out, "libsinkhorn_hip_asan.so"), link_extra=["-shared-libsan"],
+                             verbose=verbose, jobs=jobs)
 
 
 if __name__ == "__main__":

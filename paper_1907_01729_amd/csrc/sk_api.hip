@@ -16,8 +16,9 @@ sk_status check_problem(const sk_problem *p) {
     if (!p) return SK_ERR_NULLPTR;
     if (p->B < 0 || p->d1 < 1 || p->d2 < 1 || p->d1 > kMaxDim || p->d2 > kMaxDim) return SK_ERR_SHAPE;
     if (p->c_batched != 0 && p->c_batched != 1) return SK_ERR_SHAPE;
-    const int64_t cells = (int64_t)p->d1 * p->d2;
-    if (cells > (int64_t(1) << 40) || (int64_t)p->B * cells > (int64_t(1) << 46)) return SK_ERR_SHAPE;
+    const int64_t cells = (int64_t)p->d1 * p->d2;  // <= 2^48: d1, d2 <= 2^24
+    // B d1 d2 <= 2^46, tested without forming the product (it can overflow)
+    if (cells > (int64_t(1) << 40) || (int64_t)p->B > (int64_t(1) << 46) / cells) return SK_ERR_SHAPE;
     if (!sk::resident_fits(p->d1, p->d2) && !sk::tiled_fits(p->B, p->d1, p->d2, p->c_batched)) return SK_ERR_SHAPE;
     if (!(p->lambda > 0.f) || !isfinite(p->lambda)) return SK_ERR_LAMBDA;
     if (p->n_iter < 0 || !isfinite(p->tol)) return SK_ERR_ITERS;
