@@ -42,7 +42,7 @@ def _load():
         P = ctypes.c_void_p
         I = ctypes.c_int
         D = ctypes.c_double
-        lib.oracle_forward.argtypes = [I, I, I, I, D, I, D, P, P, P, P, P, P, P, P, P, P]
+        lib.oracle_forward.argtypes = [I, I, I, I, D, I, D, P, P, P, P, P, P, P, P, P, P, P]
         lib.oracle_forward.restype = I
         lib.oracle_backward.argtypes = [I, I, I, I, D, P, P, P, P, P, P, P, P, P]
         lib.oracle_backward.restype = I
@@ -84,14 +84,19 @@ def num_threads() -> int:
     return _load().oracle_num_threads()
 
 
-def forward(mu, nu, C, lam, n_iter, tol=0.0, n_iter_b=None, err_hist=False):
+def forward(mu, nu, C, lam, n_iter, tol=0.0, n_iter_b=None, err_hist=False, alpha0=None):
     """Log-domain Sinkhorn forward in fp64.
 
     Returns a dict with alpha [B,d1], beta [B,d2] (log u, log v), loss [B]
     (E^0 = sum P C), marg_err [B] (||P1-mu||_1 + ||P^T1-nu||_1), iters [B]
-    and, if requested, err_hist [B, n_iter].
+    and, if requested, err_hist [B, n_iter].  alpha0 [B,d1] (optional): a
+    warm start, log u^0 on the support of mu instead of 0 (the iteration's
+    whole state, since each iteration begins with the v-update from log u).
     """
     mu, nu, C, B, d1, d2, cb = _shapes(mu, nu, C)
+    a0 = None
+    if alpha0 is not None:
+        a0 = np.ascontiguousarray(np.asarray(alpha0, dtype=np.float64).reshape(B, d1))
     alpha = np.empty((B, d1))
     beta = np.empty((B, d2))
     loss = np.empty(B)
@@ -104,7 +109,7 @@ def forward(mu, nu, C, lam, n_iter, tol=0.0, n_iter_b=None, err_hist=False):
     hist = np.empty((B, max(n_iter, 1))) if err_hist else None
     rc = _load().oracle_forward(B, d1, d2, cb, float(lam), int(n_iter), float(tol), _ptr(nb),
                                 _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha), _ptr(beta),
-                                _ptr(loss), _ptr(merr), _ptr(iters), _ptr(hist))
+                                _ptr(loss), _ptr(merr), _ptr(iters), _ptr(hist), _ptr(a0))
     if rc != 0:
         raise ValueError("oracle_forward: invalid arguments")
     out = dict(alpha=alpha, beta=beta, loss=loss, marg_err=merr, iters=iters)

@@ -23,7 +23,11 @@
  *     logsumexp arguments sign-flipped; the batched form in Section 4 has the
  *     consistent sign, LSE_i(-C_ij/lambda + log u_i).  That form is used, and
  *     its row counterpart for the u-update.
- *   - Initialisation: log u^0 = 0 on the support of mu, -inf off it.
+ *   - Initialisation: log u^0 = 0 on the support of mu, -inf off it; or, for
+ *     a warm start (a resume of the iteration; not in the paper), a given
+ *     log u^0 on the support of mu, -inf off it.  Every iteration begins
+ *     with the v-update from log u alone, so log u is the iteration's whole
+ *     state: K iterations, then n more from their log u, are K + n.
  *   - One iteration = v-update then u-update (order of eq. (sk_plain)).
  *   - Zero mass: log u_i = -inf where mu_i = 0, log v_j = -inf where nu_j = 0
  *     (Section 3).
@@ -157,9 +161,9 @@ static void sample_forward(int d1, int d2, double lam, int n_iter, double tol,
                            const double *mu, const double *nu, const double *C,
                            double *alpha, double *beta, double *loss,
                            double *marg_err, int *iters, double *err_hist,
-                           int par)
+                           int par, const double *alpha0)
 {
-    for (int i = 0; i < d1; ++i) alpha[i] = (mu[i] > 0.0) ? 0.0 : NEG_INF;
+    for (int i = 0; i < d1; ++i) alpha[i] = (mu[i] > 0.0) ? (alpha0 ? alpha0[i] : 0.0) : NEG_INF;
     for (int j = 0; j < d2; ++j) beta[j] = (nu[j] > 0.0) ? 0.0 : NEG_INF;
     if (err_hist)
         for (int k = 0; k < n_iter; ++k) err_hist[k] = NAN;
@@ -189,13 +193,16 @@ static void sample_forward(int d1, int d2, double lam, int n_iter, double tol,
  *   n_iter_b: nullable per-sample iteration counts (overrides n_iter).
  *   outputs alpha[B*d1], beta[B*d2], loss[B], marg_err[B], iters[B];
  *   err_hist: nullable [B*n_iter].
+ *   alpha0: nullable [B*d1], the warm start's log u^0 (read on the support of
+ *   mu only; it may be the alpha array itself).
  * Returns 0, or -1 on invalid arguments.
  */
 int oracle_forward(int B, int d1, int d2, int c_batched, double lambda,
                    int n_iter, double tol, const int *n_iter_b,
                    const double *mu, const double *nu, const double *C,
                    double *alpha, double *beta, double *loss,
-                   double *marg_err, int *iters, double *err_hist)
+                   double *marg_err, int *iters, double *err_hist,
+                   const double *alpha0)
 {
     if (B < 0 || d1 < 1 || d2 < 1 || !(lambda > 0.0) || n_iter < 0) return -1;
     /* Parallelise across samples, or inside one sample's half-steps when
@@ -211,7 +218,7 @@ int oracle_forward(int B, int d1, int d2, int c_batched, double lambda,
                        alpha + (long)b * d1, beta + (long)b * d2, loss + b,
                        marg_err + b, iters + b,
                        err_hist ? err_hist + (long)b * n_iter : NULL,
-                       par_inner);
+                       par_inner, alpha0 ? alpha0 + (long)b * d1 : NULL);
     }
     return 0;
 }

@@ -22,7 +22,8 @@
 
 int oracle_forward(int B, int d1, int d2, int c_batched, double lambda, int n_iter, double tol,
                    const int *n_iter_b, const double *mu, const double *nu, const double *C, double *alpha,
-                   double *beta, double *loss, double *marg_err, int *iters, double *err_hist);
+                   double *beta, double *loss, double *marg_err, int *iters, double *err_hist,
+                   const double *alpha0);
 int oracle_backward(int B, int d1, int d2, int c_batched, double lambda, const double *grad_loss,
                     const double *mu, const double *nu, const double *C, const double *alpha, const double *beta,
                     double *grad_mu, double *grad_nu, double *grad_C);
@@ -89,7 +90,7 @@ static void run_case(int B, int d1, int d2, int cb, double lam, int n_iter, doub
     for (int b = 0; b < B; ++b) g[b] = 0.5 + urand();
 
     CHECK(oracle_forward(B, d1, d2, cb, lam, n_iter, tol, NULL, mu, nu, C, alpha, beta, loss, merr, iters,
-                         n_iter > 0 ? hist : NULL) == 0);
+                         n_iter > 0 ? hist : NULL, NULL) == 0);
     for (int b = 0; b < B; ++b) {
         const double *Cb = C + (cb ? (long)b * d1 * d2 : 0);
         const double *a = alpha + (long)b * d1, *bt = beta + (long)b * d2;
@@ -138,13 +139,28 @@ static void run_case(int B, int d1, int d2, int cb, double lam, int n_iter, doub
         double *alpha2 = malloc(sizeof(double) * (long)B * d1), *beta2 = malloc(sizeof(double) * (long)B * d2);
         int *iters2 = malloc(sizeof(int) * B);
         CHECK(oracle_forward(B, d1, d2, cb, lam, n_iter, 0.0, iters, mu, nu, C, alpha2, beta2, loss, merr, iters2,
-                             NULL) == 0);
+                             NULL, NULL) == 0);
         for (int b = 0; b < B; ++b) {
             CHECK(iters2[b] == iters[b]);
             for (int i = 0; i < d1; ++i)
                 CHECK(alpha2[(long)b * d1 + i] == alpha[(long)b * d1 + i] ||
                       (isinf(alpha2[(long)b * d1 + i]) && isinf(alpha[(long)b * d1 + i])));
         }
+        /* warm start, in place: 3 more iterations from the returned alpha
+           equal a run of iters + 3 (the state is alpha alone) */
+        int *more = malloc(sizeof(int) * B), *iters3 = malloc(sizeof(int) * B);
+        double *alpha3 = malloc(sizeof(double) * (long)B * d1);
+        for (int b = 0; b < B; ++b) more[b] = iters[b] + 3;
+        CHECK(oracle_forward(B, d1, d2, cb, lam, n_iter + 3, 0.0, more, mu, nu, C, alpha3, beta2, loss, merr,
+                             iters3, NULL, NULL) == 0);
+        for (int b = 0; b < B; ++b) more[b] = 3;
+        CHECK(oracle_forward(B, d1, d2, cb, lam, 3, 0.0, more, mu, nu, C, alpha2, beta2, loss, merr, iters2, NULL,
+                             alpha2) == 0);
+        for (long u = 0; u < (long)B * d1; ++u)
+            CHECK(alpha2[u] == alpha3[u] || (isinf(alpha2[u]) && isinf(alpha3[u])));
+        free(more);
+        free(iters3);
+        free(alpha3);
         free(alpha2);
         free(beta2);
         free(iters2);

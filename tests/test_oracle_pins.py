@@ -605,3 +605,91 @@ def test_sharp_gradient_planted_mistakes_are_caught(mutation):
     good = oracle.sharp_gradient([1.0], mu, nu, C, lam, o["alpha"], o["beta"])["grad_mu"][0] @ e
     assert fd == pytest.approx(good, rel=1e-5, abs=1e-7)
     assert abs((z - z.mean()) @ e - fd) > 1e-4, mutation
+
+
+# --------------------------------------------------------------------------
+# Warm start: a given log u^0 instead of 0 (the resume of the iteration)
+# --------------------------------------------------------------------------
+
+def _plain_sk_from(mu, nu, C, lam, n_iter, u0):
+    """eq. (sk_plain) from a given u^0: v = nu / (K^T u), then u = mu / (K v)."""
+    K = np.exp(-C / lam)
+    u = u0.copy()
+    v = np.ones(len(nu))
+    for _ in range(n_iter):
+        v = nu / (K.T @ u)
+        u = mu / (K @ v)
+    return u, v
+
+
+@pytest.mark.parametrize("n_iter", [1, 3, 8])
+def test_warm_start_matches_plain_iteration_from_u0(n_iter):
+    """A warm start is the plain iteration of eq. (sk_plain) started from
+    u^0 = exp(alpha0) (an independent algorithm): it fixes that alpha0 is the
+    start and that the first half-step is the v-update from it."""
+    rng = np.random.default_rng(17)
+    d1, d2, lam = 8, 5, 0.2
+    mu, nu = _rand_hist(rng, d1), _rand_hist(rng, d2)
+    C = rng.uniform(0, 1, (d1, d2))
+    a0 = rng.normal(0.0, 2.0, d1)
+    u, v = _plain_sk_from(mu, nu, C, lam, n_iter, np.exp(a0))
+    o = oracle.forward(mu, nu, C, lam, n_iter, alpha0=a0[None])
+    np.testing.assert_allclose(o["alpha"][0], np.log(u), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(o["beta"][0], np.log(v), rtol=1e-11, atol=1e-11)
+    cold = oracle.forward(mu, nu, C, lam, n_iter)
+    assert np.abs(cold["alpha"][0] - o["alpha"][0]).max() > 1e-6  # the start matters at finite n_iter
+
+
+def test_warm_start_resumes_the_iteration():
+    """K iterations, then n more from their alpha, are K + n iterations
+    (alpha is the whole state): identical in every bit, per sample, with zero
+    masses and a per-sample cost."""
+    rng = np.random.default_rng(23)
+    B, d1, d2, lam = 3, 9, 7, 0.1
+    mu = np.stack([_rand_hist(rng, d1) for _ in range(B)])
+    nu = np.stack([_rand_hist(rng, d2) for _ in range(B)])
+    mu[1, 2] = 0.0
+    mu[1] /= mu[1].sum()
+    nu[2, 0] = 0.0
+    nu[2] /= nu[2].sum()
+    C = rng.uniform(0, 1, (B, d1, d2))
+    first = oracle.forward(mu, nu, C, lam, 11)
+    resumed = oracle.forward(mu, nu, C, lam, 6, alpha0=first["alpha"])
+    whole = oracle.forward(mu, nu, C, lam, 17)
+    for k in ("alpha", "beta", "loss", "marg_err"):
+        np.testing.assert_array_equal(resumed[k], whole[k])
+
+
+def test_warm_start_at_the_optimum_stays_there():
+    """Started at the optimum of the entropic dual found by scipy (an
+    independent solver), one iteration keeps the plan: the marginal error
+    stays at the optimum's and the loss is the optimal plan's E^0."""
+    rng = np.random.default_rng(29)
+    d1, d2, lam = 6, 4, 0.3
+    mu, nu = _rand_hist(rng, d1), _rand_hist(rng, d2)
+    C = rng.uniform(0, 1, (d1, d2))
+    _, f, g = _scipy_dual(mu, nu, C, lam)
+    a_star = f / lam - 0.5  # log u of P = exp((f + g - C) / lam - 1), up to the gauge
+    Pref = np.exp((f[:, None] + g[None, :] - C) / lam - 1.0)
+    o = oracle.forward(mu, nu, C, lam, 1, alpha0=a_star[None])
+    assert o["marg_err"][0] <= 1e-7
+    assert o["loss"][0] == pytest.approx((Pref * C).sum(), rel=1e-7)
+    np.testing.assert_allclose(oracle.plan(C, lam, o["alpha"][0], o["beta"][0]), Pref, atol=1e-7)
+
+
+def test_warm_start_ignores_entries_off_the_support():
+    """alpha0 is read on the support of mu only: -inf off it whatever alpha0
+    holds there; a warm start from 0 on the support is the cold start."""
+    rng = np.random.default_rng(31)
+    d1, d2, lam = 7, 6, 0.2
+    mu, nu = _rand_hist(rng, d1), _rand_hist(rng, d2)
+    mu[3] = 0.0
+    mu /= mu.sum()
+    C = rng.uniform(0, 1, (d1, d2))
+    a0 = np.zeros((1, d1))
+    a0[0, 3] = 123.0
+    warm = oracle.forward(mu, nu, C, lam, 5, alpha0=a0)
+    cold = oracle.forward(mu, nu, C, lam, 5)
+    for k in ("alpha", "beta", "loss"):
+        np.testing.assert_array_equal(warm[k], cold[k])
+    assert np.isneginf(warm["alpha"][0, 3])
