@@ -148,6 +148,24 @@ SK_API sk_status sinkhorn_forward_select(const sk_problem *p, int32_t select, co
                                          size_t ws_bytes, void *stream);
 
 /*
+ * Warm start (checkpoint and resume; not in the paper): sinkhorn_forward
+ * started from the caller's row log-scalings alpha0 [B, d1] (natural log,
+ * as sinkhorn_forward returns them in alpha) on the support of mu instead of
+ * alpha = 0 there; entries off the support are ignored (-inf).  Every
+ * iteration begins with the v-update from alpha, so alpha is the iteration's
+ * whole state: continuing a K-iteration forward from its alpha for n more
+ * iterations gives the iterates of a (K + n)-iteration forward, up to
+ * rounding.  alpha0 may be the alpha output buffer itself (read before it is
+ * written).  Runs the log-domain kernels (the plain form starts from u = 1).
+ * Arguments, workspace and errors as sinkhorn_forward; alpha0 NULL:
+ * SK_ERR_NULLPTR.
+ */
+SK_API sk_status sinkhorn_forward_warm(const sk_problem *p, const float *alpha0, const float *mu,
+                                       const float *nu, const float *C, float *alpha, float *beta, float *loss,
+                                       float *marg_err, int32_t *iters, void *workspace, size_t ws_bytes,
+                                       void *stream);
+
+/*
  * Dispatch report, for logging and debugging (nothing is launched): writes
  * into buf a one-line, NUL-terminated description of the kernels and launch
  * shape that sinkhorn_forward_select(p, select, ...) takes for *p: the

@@ -39,6 +39,7 @@ EXPORTED = (
     "sinkhorn_backward_sharp",
     "sinkhorn_sharp_workspace_bytes",
     "sinkhorn_describe",
+    "sinkhorn_forward_warm",
 )
 
 
@@ -101,6 +102,8 @@ def load_library():
     lib.sinkhorn_backward_sharp.restype = ctypes.c_int
     lib.sinkhorn_sharp_workspace_bytes.argtypes = [PP]
     lib.sinkhorn_sharp_workspace_bytes.restype = ctypes.c_size_t
+    lib.sinkhorn_forward_warm.argtypes = [PP, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.sinkhorn_forward_warm.restype = ctypes.c_int
     lib.sinkhorn_describe.argtypes = [PP, I, ctypes.c_char_p, ctypes.c_size_t]
     lib.sinkhorn_describe.restype = ctypes.c_int32
     _lib = lib
@@ -180,10 +183,14 @@ def _on(stream):
     return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
 
 
-def _forward(select, mu, nu, C, lam, n_iter, tol, stream, workspace):
+def _forward(select, mu, nu, C, lam, n_iter, tol, stream, workspace, alpha0=None):
     lib = load_library()
     _dev(mu, "mu"), _dev(nu, "nu"), _dev(C, "C")
     B, d1, d2, cb = _shapes(mu, nu, C)
+    if alpha0 is not None:
+        _dev(alpha0, "alpha0")
+        if tuple(alpha0.shape) != (B, d1):
+            raise ValueError(f"alpha0 must be [B, d1] = [{B}, {d1}], got {tuple(alpha0.shape)}")
     p = problem(B, d1, d2, cb, lam, n_iter, tol)
     dev = mu.device
     f = dict(device=dev, dtype=torch.float32)
@@ -196,6 +203,13 @@ def _forward(select, mu, nu, C, lam, n_iter, tol, stream, workspace):
         need = int(lib.sinkhorn_workspace_bytes(ctypes.byref(p)))
         if workspace is None or workspace.numel() < need:
             workspace = torch.empty((max(need, 1),), device=dev, dtype=torch.uint8)
+    if alpha0 is not None:
+        st = lib.sinkhorn_forward_warm(ctypes.byref(p), _ptr(alpha0), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
+                                       _ptr(beta), _ptr(loss), _ptr(merr), _ptr(iters), _ptr(workspace),
+                                       ctypes.c_size_t(workspace.numel()), _stream(dev, stream))
+        if st != 0:
+            raise SinkhornError(st, "sinkhorn_forward_warm")
+        return dict(alpha=alpha, beta=beta, loss=loss, marg_err=merr, iters=iters)
     st = lib.sinkhorn_forward_select(ctypes.byref(p), int(select), _ptr(mu), _ptr(nu), _ptr(C), _ptr(alpha),
                                      _ptr(beta), _ptr(loss), _ptr(merr), _ptr(iters), _ptr(workspace),
                                      ctypes.c_size_t(workspace.numel()), _stream(dev, stream))
@@ -204,13 +218,16 @@ def _forward(select, mu, nu, C, lam, n_iter, tol, stream, workspace):
     return dict(alpha=alpha, beta=beta, loss=loss, marg_err=merr, iters=iters)
 
 
-def sinkhorn_forward(mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None):
+def sinkhorn_forward(mu, nu, C, lam, n_iter, tol=0.0, stream=None, workspace=None, alpha0=None):
     """Run the forward on the GPU.
 
     mu [B,d1], nu [B,d2], C [d1,d2] | [1,d1,d2] | [B,d1,d2]: float32 CUDA tensors.
+    alpha0 [B,d1] (optional): warm start from these row log-scalings (e.g. the
+    alpha of an earlier forward: n more iterations continue it), through
+    sinkhorn_forward_warm.
     Returns dict(alpha [B,d1], beta [B,d2], loss [B], marg_err [B], iters [B] int32).
     """
-    return _forward(0, mu, nu, C, lam, n_iter, tol, stream, workspace)
+    return _forward(0, mu, nu, C, lam, n_iter, tol, stream, workspace, alpha0)
 
 
 # Size of the library's fixed scratch array (SINKHORN_NOALLOC_SCRATCH_BYTES).

@@ -87,6 +87,7 @@ sk::FwdArgs fwd_args(const sk_problem *p, const float *mu, const float *nu, cons
     a.s = sk::kLog2eHost / p->lambda;
     a.select = SK_SELECT_DEFAULT;
     a.only_marked = 0;
+    a.alpha0 = nullptr;
     return a;
 }
 
@@ -235,6 +236,22 @@ sk_status sinkhorn_forward(const sk_problem *p, const float *mu, const float *nu
                            size_t ws_bytes, void *stream) {
     return sinkhorn_forward_select(p, SK_SELECT_DEFAULT, mu, nu, C, alpha, beta, loss, marg_err, iters, workspace,
                                    ws_bytes, stream);
+}
+
+sk_status sinkhorn_forward_warm(const sk_problem *p, const float *alpha0, const float *mu, const float *nu,
+                                const float *C, float *alpha, float *beta, float *loss, float *marg_err,
+                                int32_t *iters, void *workspace, size_t ws_bytes, void *stream) {
+    sk_status st = check_problem(p);
+    if (st != SK_OK) return st;
+    if (p->B == 0) return SK_OK;
+    if (!alpha0 || !mu || !nu || !C || !alpha || !beta || !loss || !marg_err || !iters) return SK_ERR_NULLPTR;
+    const size_t need = sinkhorn_workspace_bytes(p);
+    if (ws_bytes < need) return SK_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return SK_ERR_NULLPTR;
+    sk::FwdArgs a = fwd_args(p, mu, nu, C, alpha, beta, loss, marg_err, iters);
+    a.alpha0 = alpha0;
+    a.select = SK_SELECT_LOG_ONLY;  // the plain form's start is fixed at u = 1
+    return run_forward(a, workspace, static_cast<hipStream_t>(stream)) == hipSuccess ? SK_OK : SK_ERR_HIP;
 }
 
 sk_status sinkhorn_forward_noalloc(const sk_problem *p, const float *mu, const float *nu, const float *C,

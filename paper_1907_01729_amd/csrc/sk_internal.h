@@ -23,6 +23,9 @@ struct FwdArgs {
     // Set (to 1) for the log-domain launch that follows a plain-form launch of
     // the widest bucket: it solves only the problems marked with iters = -1.
     int only_marked;
+    // Warm start: alpha^0 [B, d1] (natural log) on the support of mu instead
+    // of 0; null for the cold start.  Only the log-domain kernels take it.
+    const float *alpha0;
 };
 
 struct BwdArgs {
@@ -66,6 +69,7 @@ inline FwdArgs fwd_chunk(const FwdArgs &a, int off, int n) {
     const size_t o1 = (size_t)off * a.d1, o2 = (size_t)off * a.d2;
     c.mu += o1;
     c.alpha += o1;
+    if (a.alpha0) c.alpha0 += o1;
     c.nu += o2;
     c.beta += o2;
     if (a.C && a.c_batched) c.C += o1 * a.d2;

@@ -114,8 +114,9 @@ __device__ __forceinline__ void resident_log_wave(const FwdArgs &A, float *pool)
         for (int t = 0; t < N; ++t) L[ii][t] = ((R0 + ii < rlim) && (t < tlim)) ? -s * L[ii][t] : kPadCl;
 
     // Owners: lane (p, q < H) owns row i = p + 8 (R0 + q); thread c owns
-    // column c.  a^0 = 0 on the support of mu, -inf off it (rows past d1
-    // keep 0: their cells hold kPadCl); b likewise before the first v-update.
+    // column c.  a^0 = 0 on the support of mu (a warm start's alpha^0 in
+    // base 2 there), -inf off it (rows past d1 keep 0: their cells hold
+    // kPadCl); b likewise before the first v-update.
     const bool rown = q < H;
     const int i_own = p + 8 * (R0 + q);
     const bool row_in = rown && i_own < d1;
@@ -128,6 +129,7 @@ __device__ __forceinline__ void resident_log_wave(const FwdArgs &A, float *pool)
     const int rslot = p * kVS + R0 + q;
     const int cslot = (c & 7) * kVS + (c >> 3);
     float a_own = row_in && !(ms > 0.f) ? neg_inf() : 0.f;
+    if (row_in && ms > 0.f && A.alpha0) a_own = A.alpha0[(size_t)b * d1 + i_own] * kLog2e;
     float b_own = col_in && !(ns > 0.f) ? neg_inf() : 0.f;
     if (rown) rowa[rslot] = a_own;
     if (c < 8 * N) colv[cslot] = b_own;

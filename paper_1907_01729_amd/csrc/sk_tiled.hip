@@ -59,6 +59,7 @@ struct TiledArgs {
     float *part;     // [2][R][B, d2p] column partials (plane 1 only for the exact pass)
     float *rowerr;   // [3][R][B] row-error partials: planes 0/1 by iteration parity, 2 for stats
     float *lossp;    // [R][B] loss partials (stats)
+    const float *a0;  // warm start: alpha^0 [B, d1] (natural log), else null
     int32_t *state;  // [B] 0 = running, K > 0 = stopped after iteration K
     // Early stop with a compacted batch: sync[0] counts the problems stopped
     // since the running list was last rebuilt.
@@ -96,7 +97,7 @@ __device__ __forceinline__ float block_sum(float v, float *red) { return block_s
 __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
     const size_t n = (size_t)T.B * T.d1;
     for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < n; u += (size_t)gridDim.x * kThreads)
-        T.a[u] = T.mu[u] > 0.f ? 0.f : neg_inf();
+        T.a[u] = T.mu[u] > 0.f ? (T.a0 ? T.a0[u] * kLog2e : 0.f) : neg_inf();
     // Both planes: b^0 in plane 0 (only read when n_iter == 0), zeros past d2.
     const size_t m = (size_t)2 * T.B * T.d2p;
     for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < m; u += (size_t)gridDim.x * kThreads) {
@@ -161,10 +162,11 @@ __global__ __launch_bounds__(kMergeThreads) void sk_tiled_col_exact(TiledArgs T)
     const int i0 = r * T.RBS, i1 = min(T.d1, i0 + T.RBS);
     const float *Cb = T.C ? T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0) : nullptr;
     const float *mub = T.mu + (size_t)b * T.d1;
+    const float *ab = T.a + (size_t)b * T.d1;
     float m = kNegBig, s = 0.f;
     for (int i = i0; i < i1; ++i) {
         if (!(mub[i] > 0.f)) continue;  // a^0 = -inf: contributes nothing
-        const float x = cl_at(T, Cb, b, i, j);
+        const float x = ab[i] + cl_at(T, Cb, b, i, j);  // a^0 = 0 unless warm-started
         const float mn = fmaxf(m, x);
         s = s * ex2(m - mn) + ex2(x - mn);
         m = mn;
@@ -1761,6 +1763,7 @@ TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     T.D = 0;
     T.rs = 0.f;
     T.a = a.alpha;
+    T.a0 = a.alpha0;
     T.a2 = nullptr;
     T.bbuf = reinterpret_cast<float *>(base + L.bbuf);
     T.part = reinterpret_cast<float *>(base + L.part);

@@ -14,8 +14,9 @@ from ._binding import (sinkhorn_backward, sinkhorn_backward_points, sinkhorn_bac
 
 class SinkhornLoss(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, mu, nu, C, lam, n_iter, tol, sharp=False):
-        out = sinkhorn_forward(mu.contiguous(), nu.contiguous(), C.contiguous(), lam, n_iter, tol)
+    def forward(ctx, mu, nu, C, lam, n_iter, tol, sharp=False, alpha0=None):
+        out = sinkhorn_forward(mu.contiguous(), nu.contiguous(), C.contiguous(), lam, n_iter, tol,
+                               alpha0=None if alpha0 is None else alpha0.detach().contiguous())
         ctx.save_for_backward(mu, nu, C, out["alpha"], out["beta"])
         ctx.lam = lam
         ctx.sharp = sharp
@@ -31,22 +32,23 @@ class SinkhornLoss(torch.autograd.Function):
                 raise NotImplementedError("the sharp gradient is taken with respect to mu and nu only")
             g = sinkhorn_backward_sharp(grad_loss.contiguous(), mu.contiguous(), nu.contiguous(), C.contiguous(),
                                         ctx.lam, alpha, beta)
-            return g["grad_mu"], g["grad_nu"], None, None, None, None, None
+            return g["grad_mu"], g["grad_nu"], None, None, None, None, None, None
         g = sinkhorn_backward(grad_loss.contiguous(), mu.contiguous(), nu.contiguous(), C.contiguous(), ctx.lam,
                               alpha, beta, grad_C=want_C)
         gC = None
         if want_C:
             gC = g["grad_C"].reshape(C.shape) if C.dim() == 3 or g["grad_C"].shape[0] == 1 else g["grad_C"]
             gC = gC.reshape(C.shape)
-        return g["grad_mu"], g["grad_nu"], gC, None, None, None, None
+        return g["grad_mu"], g["grad_nu"], gC, None, None, None, None, None
 
 
-def sinkhorn_loss(mu, nu, C, lam, n_iter, tol=0.0, return_state=False, sharp=False):
+def sinkhorn_loss(mu, nu, C, lam, n_iter, tol=0.0, return_state=False, sharp=False, alpha0=None):
     """Per-sample loss E^0 [B]; differentiable w.r.t. mu, nu and C.  By default
     the backward is the multiplier gradient of E^lambda (Section 5's choice);
-    sharp=True differentiates E^0 itself through the plan (mu and nu only,
-    max(d1, d2) <= 128)."""
-    loss, alpha, beta, merr, iters = SinkhornLoss.apply(mu, nu, C, lam, n_iter, tol, sharp)
+    sharp=True differentiates E^0 itself through the plan (mu and nu only).
+    alpha0 [B, d1] (optional): warm start of the iteration, e.g. from the
+    state of the previous step (return_state=True), treated as a constant."""
+    loss, alpha, beta, merr, iters = SinkhornLoss.apply(mu, nu, C, lam, n_iter, tol, sharp, alpha0)
     if return_state:
         return loss, dict(alpha=alpha, beta=beta, marg_err=merr, iters=iters)
     return loss

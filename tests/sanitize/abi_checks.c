@@ -105,12 +105,16 @@ int main(void)
         CHECK(sinkhorn_forward_select(p, 9, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_ERR_ARG);
         /* NULL arrays */
         CHECK(sinkhorn_forward(p, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_ERR_NULLPTR);
+        CHECK(sinkhorn_forward_warm(p, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_ERR_NULLPTR);
         CHECK(sinkhorn_backward(p, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_ERR_NULLPTR);
         CHECK(sinkhorn_forward_points(p, 3, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_ERR_NULLPTR);
         /* a workspace one byte short, placeholder pointers: rejected before launch */
-        if (ws > 0)
+        if (ws > 0) {
             CHECK(sinkhorn_forward(p, fake, fake, fake, fake, fake, fake, fake, ifake, fake, ws - 1, NULL) ==
                   SK_ERR_WORKSPACE);
+            CHECK(sinkhorn_forward_warm(p, fake, fake, fake, fake, fake, fake, fake, fake, ifake, fake, ws - 1,
+                                        NULL) == SK_ERR_WORKSPACE);
+        }
         const size_t sws = sinkhorn_sharp_workspace_bytes(p);
         if (sws > 0)
             CHECK(sinkhorn_backward_sharp(p, fake, fake, fake, fake, fake, fake, fake, fake, 10, 1e-6f, ifake,
@@ -129,6 +133,7 @@ int main(void)
     /* an empty batch succeeds without touching any pointer */
     const sk_problem empty = prob(0, 10, 10, 0, 0.1f, 10, 0.f);
     CHECK(sinkhorn_forward(&empty, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_OK);
+    CHECK(sinkhorn_forward_warm(&empty, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_OK);
     CHECK(sinkhorn_backward(&empty, 0, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_OK);
     CHECK(sinkhorn_forward_noalloc(&empty, 0, 0, 0, 0, 0, 0, 0, 0, NULL) == SK_OK);
 

@@ -246,3 +246,18 @@ def test_describe_truncates_and_rejects():
     assert lib.sinkhorn_describe(ctypes.byref(p), 0, None, 8) == -1
     with pytest.raises(_binding.SinkhornError):
         sk.sinkhorn_describe(4, 10, 10, 0, lam=0.0)
+
+
+def test_warm_start_rejections_on_host():
+    lib = sk.load_library()
+    v = None
+
+    def call(p, ptr=None, ws=0):
+        a = ctypes.c_void_p(ptr) if ptr else None
+        return lib.sinkhorn_forward_warm(ctypes.byref(p), a, a, a, a, a, a, a, a, a, a, ctypes.c_size_t(ws), None)
+    assert call(_binding.problem(4, 10, 10, 0, 0.1, 10)) == -1  # alpha0 and the arrays are NULL
+    assert call(_binding.problem(0, 10, 10, 0, 0.1, 10)) == 0   # empty batch
+    assert call(_binding.problem(4, 10, 10, 0, 0.0, 10)) == -3
+    assert call(_binding.problem(4, 10, 10, 0, 0.1, -2)) == -4
+    need = sk.sinkhorn_workspace_bytes(8, 784, 784, 0, 0.01, 10)
+    assert call(_binding.problem(8, 784, 784, 0, 0.01, 10), ptr=0x1000, ws=need - 1) == -5
