@@ -154,25 +154,56 @@ __device__ __forceinline__ float cl_at(const TiledArgs &T, const float *Cb, int 
 
 // v-update of iteration 1, per row block: online (max, sumexp) of
 // a^0_i + cl_ij over the block's rows for every column j (one thread per
-// (problem, column), reading cost rows coalesced across threads).
+// column, reading cost rows coalesced across threads; the work-group is one
+// wavefront).  A shared cost is read once for W problems: each thread carries
+// the W problems' (max, sum) pairs, each updated in row order as alone.  The
+// row potentials of 64 rows are loaded one per lane (-inf at zero mass: the
+// row contributes nothing) and read with readlane, so the row loop waits on
+// no scalar load.
+template <int W>
 __global__ __launch_bounds__(kMergeThreads) void sk_tiled_col_exact(TiledArgs T) {
-    const int j = blockIdx.x * kMergeThreads + threadIdx.x;
-    const int r = blockIdx.y, b = blockIdx.z;
-    if (j >= T.d2) return;
+    const int lane = threadIdx.x;
+    const int j = blockIdx.x * kMergeThreads + lane;
+    const int r = blockIdx.y, b0 = blockIdx.z * W;
     const int i0 = r * T.RBS, i1 = min(T.d1, i0 + T.RBS);
-    const float *Cb = T.C ? T.C + (T.c_batched ? (size_t)b * T.d1 * T.d2 : 0) : nullptr;
-    const float *mub = T.mu + (size_t)b * T.d1;
-    const float *ab = T.a + (size_t)b * T.d1;
-    float m = kNegBig, s = 0.f;
-    for (int i = i0; i < i1; ++i) {
-        if (!(mub[i] > 0.f)) continue;  // a^0 = -inf: contributes nothing
-        const float x = ab[i] + cl_at(T, Cb, b, i, j);  // a^0 = 0 unless warm-started
-        const float mn = fmaxf(m, x);
-        s = s * ex2(m - mn) + ex2(x - mn);
-        m = mn;
+    const bool col_in = j < T.d2;
+    const float *Cb = T.C ? T.C + (T.c_batched ? (size_t)b0 * T.d1 * T.d2 : 0) : nullptr;
+    float m[W], s[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        m[w] = kNegBig;
+        s[w] = 0.f;
     }
-    T.part[pidx(T, 0, r, b, j)] = m;
-    T.part[pidx(T, 1, r, b, j)] = s;
+    for (int c0 = i0; c0 < i1; c0 += 64) {
+        float av[W];  // a^0 of row c0 + lane (0 unless warm-started), -inf at zero mass
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const size_t u = (size_t)(b0 + w) * T.d1 + c0 + lane;
+            av[w] = b0 + w < T.B && c0 + lane < i1 && T.mu[u] > 0.f ? T.a[u] : neg_inf();
+        }
+        const int n = min(64, i1 - c0);
+        for (int q = 0; q < n; ++q) {
+            const int i = c0 + q;
+            // W > 1: a shared cost, the same for every problem
+            const float cl = col_in ? (W > 1 ? -T.s * Cb[(size_t)i * T.d2 + j] : cl_at(T, Cb, b0, i, j)) : 0.f;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                const float aw = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(av[w]), q));
+                if (aw == neg_inf()) continue;  // wavefront-uniform
+                const float x = aw + cl;
+                const float mn = fmaxf(m[w], x);
+                s[w] = s[w] * ex2(m[w] - mn) + ex2(x - mn);
+                m[w] = mn;
+            }
+        }
+    }
+    if (!col_in) return;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        if (b0 + w >= T.B) break;
+        T.part[pidx(T, 0, r, b0 + w, j)] = m[w];
+        T.part[pidx(T, 1, r, b0 + w, j)] = s[w];
+    }
 }
 
 // Exact logsumexp (base 2) over all rows i of a_i + cl_ij for one column:
@@ -1413,24 +1444,42 @@ __global__ __launch_bounds__(64 * StreamShape<NC4>::W) void sk_tiled_sweep_strea
 }
 
 // Outputs of the returned iterate: marginal error, E^0, natural-log potentials.
-__global__ __launch_bounds__(kThreads) void sk_tiled_final(TiledArgs T) {
-    __shared__ float red[kWaves];
+template <int NT>
+__global__ __launch_bounds__(NT) void sk_tiled_final(TiledArgs T) {
+    __shared__ float red[NT / 64];
     const int b = blockIdx.x;
     const int st = T.state[b];
     const int K = st ? st : T.n_iter;
     const float *bsrc = T.bbuf + (size_t)(K & 1) * T.B * T.d2p + (size_t)b * T.d2p;
+    const size_t rstride = (size_t)T.B * T.d2p / 4;  // one row block, in f4v
     float colerr = 0.f;
-    for (int j = threadIdx.x; j < T.d2; j += kThreads) {
-        float cs = 0.f;
-        for (int r = 0; r < T.R; ++r) cs += T.part[pidx(T, 0, r, b, j)];
-        colerr += fabsf(cs - T.nu[(size_t)b * T.d2 + j]);
-        T.beta_out[(size_t)b * T.d2 + j] = bsrc[j] * kLn2;
+    // Column sums of the returned plan over the row blocks (in block order,
+    // 16 loads in flight), four consecutive columns per thread.
+    for (int j0 = 4 * threadIdx.x; j0 < T.d2; j0 += 4 * NT) {
+        const f4v *col = reinterpret_cast<const f4v *>(T.part + pidx(T, 0, 0, b, j0));
+        f4v cs = {0.f, 0.f, 0.f, 0.f};
+        for (int r0 = 0; r0 < T.R; r0 += 16) {
+            f4v v[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                v[q] = r0 + q < T.R ? col[(size_t)(r0 + q) * rstride] : f4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 16; ++q) cs += v[q];
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int j = j0 + c;
+            if (j < T.d2) {
+                colerr += fabsf(cs[c] - T.nu[(size_t)b * T.d2 + j]);
+                T.beta_out[(size_t)b * T.d2 + j] = bsrc[j] * kLn2;
+            }
+        }
     }
-    for (int i = threadIdx.x; i < T.d1; i += kThreads) {
+    for (int i = threadIdx.x; i < T.d1; i += NT) {
         const size_t u = (size_t)b * T.d1 + i;
         T.alpha_out[u] = aplane(T, K)[u] * kLn2;
     }
-    colerr = block_sum(colerr, red);
+    colerr = block_sum_n<NT>(colerr, red);
     if (threadIdx.x == 0) {
         float re = 0.f, lo = 0.f;
         for (int r = 0; r < T.R; ++r) {
@@ -1573,8 +1622,21 @@ hipError_t allow_lds(Kernel *kernel, size_t bytes) {
                                (int)bytes);
 }
 
-// Launch sequence: init, exact first v-update (+ merge), n sweeps with a merge
-// after each but the last, stats sweep, final.
+// The exact first v-update (a shared cost read once for 8 problems) and the
+// closing kernel (1024 threads per problem above 1024 columns).
+void launch_col_exact(const TiledArgs &T, hipStream_t st) {
+    if (!T.c_batched && !T.X && T.B >= 8)
+        hipLaunchKernelGGL(sk_tiled_col_exact<8>, dim3(T.JC, T.R, (T.B + 7) / 8), dim3(kMergeThreads), 0, st, T);
+    else
+        hipLaunchKernelGGL(sk_tiled_col_exact<1>, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+}
+void launch_final(const TiledArgs &T, hipStream_t st) {
+    if (T.d2 > 1024)
+        hipLaunchKernelGGL(sk_tiled_final<1024>, dim3(T.B), dim3(1024), 0, st, T);
+    else
+        hipLaunchKernelGGL(sk_tiled_final<256>, dim3(T.B), dim3(256), 0, st, T);
+}
+
 // Launch sequence of the wide rows: as run_sequence, each sweep being a rows
 // pass and a columns pass.
 hipError_t run_wide(const TiledArgs &T, hipStream_t st) {
@@ -1582,7 +1644,7 @@ hipError_t run_wide(const TiledArgs &T, hipStream_t st) {
     const dim3 rg(T.R, T.B), cg(T.d2p / kThreads, T.R, T.B);
     hipLaunchKernelGGL(sk_tiled_init, dim3(512), blk, 0, st, T);
     if (T.n_iter > 0) {
-        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+        launch_col_exact(T, st);
         hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), dim3(kMergeThreads), 0, st, T);
         for (int k = 1; k <= T.n_iter; ++k) {
             hipLaunchKernelGGL(sk_wide_rows<false>, rg, rblk, 0, st, T, k);
@@ -1592,16 +1654,18 @@ hipError_t run_wide(const TiledArgs &T, hipStream_t st) {
     }
     hipLaunchKernelGGL(sk_wide_rows<true>, rg, rblk, 0, st, T, 0);
     hipLaunchKernelGGL(sk_wide_cols<true>, cg, blk, 0, st, T, 0);
-    hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), blk, 0, st, T);
+    launch_final(T, st);
     return hipGetLastError();
 }
 
+// Launch sequence: init, exact first v-update (+ merge), n sweeps with a merge
+// after each but the last, stats sweep, final.
 template <class Sweep, class Stats>
 hipError_t run_sequence(const TiledArgs &T, hipStream_t st, Sweep sweep, Stats stats) {
     const dim3 blk(kThreads);
     hipLaunchKernelGGL(sk_tiled_init, dim3(512), blk, 0, st, T);
     if (T.n_iter > 0) {
-        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+        launch_col_exact(T, st);
         const dim3 mblk(kMergeThreads);
         hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), mblk, 0, st, T);
         for (int k = 1; k <= T.n_iter; ++k) {
@@ -1616,7 +1680,7 @@ hipError_t run_sequence(const TiledArgs &T, hipStream_t st, Sweep sweep, Stats s
         }
     }
     stats();
-    hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), blk, 0, st, T);
+    launch_final(T, st);
     return hipGetLastError();
 }
 
@@ -1642,13 +1706,13 @@ hipError_t run_stream(const TiledArgs &T, hipStream_t st) {
     const dim3 grid(T.R, T.B), blk(64 * W);
     hipLaunchKernelGGL(sk_tiled_init, dim3(512), dim3(kThreads), 0, st, T);
     if (T.n_iter > 0) {
-        hipLaunchKernelGGL(sk_tiled_col_exact, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
+        launch_col_exact(T, st);
         hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), dim3(kMergeThreads), 0, st, T);
         for (int k = 1; k <= T.n_iter; ++k)
             hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, false>), grid, blk, lds, st, T, k);
     }
     hipLaunchKernelGGL((sk_tiled_sweep_stream<NC4, true>), grid, blk, lds, st, T, 0);
-    hipLaunchKernelGGL(sk_tiled_final, dim3(T.B), dim3(kThreads), 0, st, T);
+    launch_final(T, st);
     return hipGetLastError();
 }
 
