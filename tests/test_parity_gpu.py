@@ -749,6 +749,29 @@ def test_wide_grid_image_sampled():
     check_backward(prob, gpu, ref, idx=idx)
 
 
+@pytest.mark.parametrize("B,d1,d2", [(6, 40, 30), (5, 300, 260), (4, 150, 4100)])
+def test_non_finite_cost_propagates(B, d1, d2):
+    """A NaN in one problem's cost (per-sample costs): that problem's loss and
+    error are not finite and it runs every iteration (its error is never
+    <= tol); every other problem is bit-identical to a run without the NaN.
+    A NaN in a shared cost makes every problem's loss non-finite.  Every call
+    returns: the loops are bounded by the shapes and n_iter, never by the
+    data."""
+    prob = workloads.random_problem(seed=88, B=B, d1=d1, d2=d2, lam=0.1, n_iter=30, c_batched=True, tol=1e-5)
+    clean = _gpu(prob)
+    prob.C[2, d1 // 2, d2 // 3] = np.nan
+    dirty = _gpu(prob)
+    assert not np.isfinite(dirty["loss"][2]) and not np.isfinite(dirty["marg_err"][2])
+    assert dirty["iters"][2] == prob.n_iter
+    others = [b for b in range(B) if b != 2]
+    for k in ("alpha", "beta", "loss", "marg_err", "iters"):
+        np.testing.assert_array_equal(dirty[k][others], clean[k][others])
+    shared = workloads.random_problem(seed=89, B=8, d1=d1, d2=d2, lam=0.1, n_iter=20, tol=1e-5)
+    shared.C[0, 0, 0] = np.nan
+    out = _gpu(shared)
+    assert not np.any(np.isfinite(out["loss"])) and np.all(out["iters"] == shared.n_iter)
+
+
 def test_shared_grad_C_many_rows():
     """A shared cost with d1 = 70000 rows (more than a grid's y dimension):
     the forward runs in the tiled regime and grad_C (rows grid-strided) covers
