@@ -93,9 +93,9 @@ def kernel_source_hash(files):
     return h.hexdigest()[:16]
 
 
-def stored_traffic(profile_name, src_hash):
-    """HBM bytes per launch from a committed rocprofv3 --pmc summary, if it was
-    taken on the current kernel source (else None)."""
+def stored_counters(profile_name, src_hash):
+    """The JSON block of a committed rocprofv3 --pmc summary, if it was taken
+    on the current kernel source (else None)."""
     path = os.path.join(ROOT, "profiles", profile_name)
     if not os.path.exists(path):
         return None
@@ -103,9 +103,24 @@ def stored_traffic(profile_name, src_hash):
     if not m:
         return None
     d = json.loads(m.group(1))
-    if d.get("source_hash") != src_hash:
-        return None
-    return d.get("hbm_bytes_per_launch")
+    return d if d.get("source_hash") == src_hash else None
+
+
+def stored_traffic(profile_name, src_hash):
+    """HBM bytes per launch from a committed counter summary (None if stale)."""
+    d = stored_counters(profile_name, src_hash)
+    return d.get("hbm_bytes_per_launch") if d else None
+
+
+def counter_fields(profile_name, src_hash):
+    """Issue utilisation of the dominant kernel from its committed counter
+    summary (None if stale): the share of the SIMDs' cycles spent issuing
+    vector instructions (4 cycles per fp32 wave64 instruction, 8 per
+    transcendental one), and the exp issue rate against 19.66 Texp/s."""
+    d = stored_counters(profile_name, src_hash)
+    if not d:
+        return dict(valu_busy=None, exp_issue_frac=None)
+    return dict(valu_busy=d.get("valu_busy_est"), exp_issue_frac=d.get("exp_issue_frac"))
 
 
 # The oracle's baseline repeats whole passes of its sample until at least this
@@ -326,7 +341,8 @@ def main():
         src = kernel_source_hash(["sk_resident.hip", "sk_resident_log.h", "sk_resident_gen.h", "sk_device.h"])
         roof = dict(bound="alu", achieved=round(achieved, 4), peak=round(PEAK_EXP_TS, 4), unit="Texp/s",
                     frac=round(achieved / PEAK_EXP_TS, 4),
-                    traffic=stored_traffic(f"{kname}_{prob.name}_counters.md", src), kernel=kname,
+                    traffic=stored_traffic(f"{kname}_{prob.name}_counters.md", src),
+                    **counter_fields(f"{kname}_{prob.name}_counters.md", src), kernel=kname,
                     kernel_ms=round(kernel_ms, 5), work="exp2 per launch = (iters + 2)*d1*d2 per problem")
     elif regime == 1:
         # Resident regime: the first-choice plain-form kernel solves every
@@ -350,7 +366,9 @@ def main():
         src = kernel_source_hash([*kfiles, "sk_device.h"])
         traffic = stored_traffic(f"{kname}_{prob.name}_counters.md", src)
         roof = dict(bound=bound, achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
-                    frac=round(achieved / peak, 4), traffic=traffic, kernel=kname, kernel_ms=round(kernel_ms, 5),
+                    frac=round(achieved / peak, 4), traffic=traffic,
+                    **counter_fields(f"{kname}_{prob.name}_counters.md", src), kernel=kname,
+                    kernel_ms=round(kernel_ms, 5),
                     work="fp32 flops per launch = (4*iters + 6)*d1*d2 per problem")
     else:
         # Tiled regime: the dominant kernel is the sweep (one pass over the
@@ -401,6 +419,7 @@ def main():
                         frac=round(achieved / PEAK_EXP_TS, 4), kernel=kname + " + sk_tiled_merge_cols",
                         kernel_ms=round(kernel_ms, 5), work="exp2 per iteration = B*d1*d2 (one per cell)")
         roof["traffic"] = stored_traffic(f"{kname}_{prob.name}_counters.md", src)
+        roof.update(counter_fields(f"{kname}_{prob.name}_counters.md", src))
         roof["sweep_timing"] = f"(t_fwd(n={n_hi}) - t_fwd(n={n_lo})) / {sweeps:g} sweeps, events on the library stream"
 
     res = {
