@@ -23,13 +23,17 @@
 //   sweep(k), merge(k)   k = 1..n (no merge after the last sweep)
 //   sweep(stats), final  loss E^0 and marginal error of the returned iterate,
 //                        outputs in natural-log units
-// Early stop (tol > 0): the merge of problem b holds b's whole error after
-// iteration k (column part summed there, row part from the sweep's
-// double-buffered row-block partials) and records K = k in the stop flag,
+// Early stop (tol > 0): the merge of problem b gathers b's whole error after
+// iteration k (column part summed there, by several work-groups above 1024
+// columns that combine their parts in one fixed-point atomic; row part from
+// the sweep's double-buffered row-block partials) and records K = k in the
+// stop flag,
 // which every later sweep and merge honours.  In the streaming sweep every
 // work-group of b sums the same partials in the same order, so all take the
 // same decision, and the first row block records it.
 #include <stdio.h>
+
+#include <cmath>
 
 #include "sk_device.h"
 #include "sk_internal.h"
@@ -40,6 +44,8 @@ namespace {
 constexpr int kThreads = 256;  // 4 wavefronts per work-group
 constexpr int kWaves = kThreads / 64;
 constexpr int kMergeThreads = 64;  // merge: one wavefront per (problem, 64 columns)
+constexpr int kMergeColsThreads = 256;  // merge after a sweep: 4 columns per thread
+constexpr int kFxCountShift = 49;       // split merge's stop accumulator: count above, sum below
 constexpr float kPadCost = -1.0e30f;  // cost of cells beyond d2: plan entry 0, finite so 0*cl = 0
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" seed of the online max
 
@@ -68,6 +74,15 @@ struct TiledArgs {
     // null): order[0, nlive) lists the running problems in increasing order;
     // the identity at first, rebuilt by the merge after a problem stops.
     int32_t *order, *nlive;
+    // Merge split into MS work-groups per problem (MS > 1, early stop only):
+    // each adds its share of the marginal error, in fixed point, and a count
+    // of one to stopacc[b] in one 64-bit atomic; the one that completes the
+    // count takes the stop decision (see sk_tiled_merge_cols).
+    unsigned long long *stopacc;
+    int MS;
+    float fx_cap;     // parts are clamped to [0, fx_cap] (NaN counts as fx_cap)
+    double fx_scale;  // fixed-point units per unit of error
+    double fx_tol;    // tol in fixed-point units
     float *alpha_out, *beta_out, *loss_out, *merr_out;
     int32_t *iters_out;
     int B, d1, d2, R, RBS, JC, n_iter, c_batched;
@@ -110,6 +125,7 @@ __global__ __launch_bounds__(kThreads) void sk_tiled_init(TiledArgs T) {
     for (size_t u = (size_t)blockIdx.x * kThreads + threadIdx.x; u < (size_t)T.B; u += (size_t)gridDim.x * kThreads) {
         T.state[u] = 0;
         if (T.order) T.order[u] = (int32_t)u;
+        if (T.stopacc) T.stopacc[u] = 0;
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         T.sync[0] = 0;
@@ -266,23 +282,32 @@ __device__ void relist_running(const TiledArgs &T) {
     if (threadIdx.x == 0) *T.nlive = base;
 }
 
-// Merge after sweep k (k < n_iter), one work-group per problem: column sums
-// of the plan after the u-update of iteration k, summed over the row blocks in
-// a fixed order; the v-update of iteration k+1; iterate k's marginal error.
-// Each thread takes groups of four consecutive columns (16-byte loads of the
-// padded rows; padding columns keep 0).
+// Merge after sweep k (k < n_iter), work-group (b, slice) for problem b's
+// columns [4 NT slice, 4 NT (slice + 1)): column sums of the plan after the
+// u-update of iteration k, summed over the row blocks in a fixed order; the
+// v-update of iteration k+1; iterate k's marginal error.  Each thread takes one
+// group of four consecutive columns (16-byte loads of the padded rows; padding
+// columns keep 0).
 //
-// Early stop (tol > 0): the work-group holds problem b's whole error (column
-// part summed here, row part from the sweep's row-block partials), so it stops
-// b at K = k when the error is <= tol without any exchange with other
-// work-groups; every later launch skips b.  With a compacted batch, stops are
-// counted in sync[0], and one extra work-group (index B) rebuilds the running
-// list from the stops of earlier launches when the count is nonzero.
+// Early stop (tol > 0): problem b's error is the column part summed here plus
+// the row part from the sweep's row-block partials (added by slice 0).  With
+// one slice the work-group stops b at K = k when the error is <= tol.  With
+// MS slices each adds its part to stopacc[b] in one 64-bit atomic: bits 0..48
+// hold the sum in fixed point (integer addition, so the total has the same
+// bits whatever the order of arrival), bits 49..63 count the slices.  The
+// slice whose add completes the count takes the decision from the sum; no
+// work-group waits for another, and no other memory is shared between them.
+// Parts are clamped to fx_cap >= 2 tol, which leaves every decision unchanged
+// (a clamped part alone exceeds tol).  Every later launch skips a stopped b.
+// With a compacted batch, stops are counted in sync[0], and one extra
+// work-group (index B, slice 0) rebuilds the running list from the stops of
+// earlier launches when the count is nonzero.
 template <int NT>
 __global__ __launch_bounds__(NT) void sk_tiled_merge_cols(TiledArgs T, int k) {
     __shared__ float red[NT / 64];
-    const int b = blockIdx.x;
+    const int b = blockIdx.x, sl = blockIdx.y;
     if (b == T.B) {  // the relist work-group of a compacted batch
+        if (sl != 0) return;
         const int seen = T.sync[0];
         if (seen == 0) return;  // nothing stopped since the last rebuild
         relist_running<NT>(T);
@@ -292,7 +317,8 @@ __global__ __launch_bounds__(NT) void sk_tiled_merge_cols(TiledArgs T, int k) {
     if (T.state[b] != 0) return;  // block-uniform
     const size_t rstride = (size_t)T.B * T.d2p / 4;  // one row block, in f4v
     float err = 0.f;
-    for (int j0 = 4 * threadIdx.x; j0 < T.d2; j0 += 4 * NT) {
+    const int j0 = 4 * (sl * NT + (int)threadIdx.x);
+    if (j0 < T.d2) {
         const f4v *col = reinterpret_cast<const f4v *>(T.part + pidx(T, 0, 0, b, j0));
         f4v cs = {0.f, 0.f, 0.f, 0.f};
         for (int r0 = 0; r0 < T.R; r0 += 16) {
@@ -325,10 +351,23 @@ __global__ __launch_bounds__(NT) void sk_tiled_merge_cols(TiledArgs T, int k) {
         *reinterpret_cast<f4v *>(T.bbuf + (size_t)((k + 1) & 1) * T.B * T.d2p + (size_t)b * T.d2p + j0) = bnew;
     }
     if (!(T.tol > 0.f)) return;
-    const float *re = T.rowerr + (size_t)(k & 1) * T.R * T.B;
-    for (int q = threadIdx.x; q < T.R; q += NT) err += re[(size_t)q * T.B + b];
+    if (sl == 0) {
+        const float *re = T.rowerr + (size_t)(k & 1) * T.R * T.B;
+        for (int q = threadIdx.x; q < T.R; q += NT) err += re[(size_t)q * T.B + b];
+    }
     err = block_sum_n<NT>(err, red);
-    if (threadIdx.x == 0 && err <= T.tol) {
+    if (threadIdx.x != 0) return;
+    bool stop = err <= T.tol;
+    if (T.MS > 1) {
+        const float part = err <= T.fx_cap ? err : T.fx_cap;  // NaN -> fx_cap
+        const unsigned long long add =
+            (1ull << kFxCountShift) + (unsigned long long)__builtin_rint((double)part * T.fx_scale);
+        const unsigned long long got = atomicAdd(T.stopacc + b, add) + add;
+        if ((got >> kFxCountShift) != (unsigned long long)T.MS) return;
+        T.stopacc[b] = 0;  // for the next merge (a later launch)
+        stop = (double)(got & ((1ull << kFxCountShift) - 1ull)) <= T.fx_tol;
+    }
+    if (stop) {
         T.state[b] = k;
         if (T.order) atomicAdd(&T.sync[0], 1);
     }
@@ -876,6 +915,18 @@ __device__ __forceinline__ float lane_get(float v, int src) {
     return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
 }
 
+// s_setprio with a level known only after unrolling (0..3).
+__device__ __forceinline__ void set_issue_priority(int p) {
+    if (p <= 0)
+        __builtin_amdgcn_s_setprio(0);
+    else if (p == 1)
+        __builtin_amdgcn_s_setprio(1);
+    else if (p == 2)
+        __builtin_amdgcn_s_setprio(2);
+    else
+        __builtin_amdgcn_s_setprio(3);
+}
+
 template <int NCW, int W, int RS, int RB, bool VEC4, bool STATS>
 __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int k) {
     constexpr int D2P = NCW * 64;  // LDS row length (columns beyond d2 hold kPadC)
@@ -1016,10 +1067,12 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                     read_group(0);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                // The exponentials at the lowest issue priority, the batch's
-                // serial reduction and update at the highest, so that another
-                // wavefront's exponentials fill this one's reduction latency.
-                __builtin_amdgcn_s_setprio(0);
+                // Issue priority falls with the batch's place in the chunk
+                // (3 for the first rows, 0 for the last): of the wavefronts
+                // sharing a SIMD, the one behind issues first, so they reach
+                // the chunk's barrier together instead of the oldest one
+                // finishing early and leaving the SIMD to the other.
+                set_issue_priority(3 - rb * 4 / RS);
 #pragma unroll
                 for (int g = 0; g < NG; ++g) {
                     if (g + 1 < NG) read_group(g + 1);
@@ -1036,7 +1089,6 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                 }
 #pragma unroll
                 for (int q = 0; q < RB; ++q) p[q] = tree_sum<NCW>(e[q]);
-                __builtin_amdgcn_s_setprio(3);
                 // Row updates of the batch, one row per 16-lane group (the
                 // all-reduce's packed layout): each lane fetches its row's
                 // potential and mass from the segment registers.
@@ -1074,12 +1126,10 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                         RB == 1 ? (upd ? an : av) : lane_get(upd ? an : av, lane_of_row<RB>(dq >= 0 && dq < RB ? dq : 0));
                     a_out = dq >= 0 && dq < RB ? got : a_out;
                 }
-                __builtin_amdgcn_s_setprio(0);
 #pragma unroll
                 for (int q = 0; q < RB; ++q)
 #pragma unroll
                     for (int c = 0; c < NCW; ++c) colpart[c] = __builtin_fmaf(e[q][c], f[q], colpart[c]);
-                __builtin_amdgcn_s_setprio(3);
                 if (!STATS && exact_any) {
 #pragma unroll
                     for (int q = 0; q < RB; ++q) {
@@ -1558,7 +1608,7 @@ void row_blocks(int B, int d1, int d2, int kind, int *R, int *RBS) {
 }
 
 struct Layout {
-    size_t bbuf, part, rowerr, lossp, state, order, a2, ctr, total;
+    size_t bbuf, part, rowerr, lossp, state, order, a2, ctr, stopacc, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1584,6 +1634,9 @@ int padded_width(int d2, int kind) {
     return w;
 }
 
+// Work-groups per problem of the merge after a sweep (4 columns per thread).
+int merge_slices(int d2) { return (d2 + 4 * kMergeColsThreads - 1) / (4 * kMergeColsThreads); }
+
 Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC_out) {
     int R, RBS;
     row_blocks(B, d1, d2, kind, &R, &RBS);
@@ -1607,6 +1660,8 @@ Layout layout(int B, int d1, int d2, int kind, int *R_out, int *RBS_out, int *JC
     if (stream_shape(d2, kind)) off = align256(off + sizeof(float) * (size_t)B * d1);
     L.ctr = off;
     if (kind == kKindPoints) off = align256(off + sizeof(float) * 4 * (size_t)B);
+    L.stopacc = off;  // stopacc[B] (split merges only)
+    if (merge_slices(d2) > 1) off = align256(off + sizeof(unsigned long long) * (size_t)B);
     L.total = off;
     if (R_out) *R_out = R;
     if (RBS_out) *RBS_out = RBS;
@@ -1630,6 +1685,12 @@ void launch_col_exact(const TiledArgs &T, hipStream_t st) {
     else
         hipLaunchKernelGGL(sk_tiled_col_exact<1>, dim3(T.JC, T.R, T.B), dim3(kMergeThreads), 0, st, T);
 }
+// MS = ceil(d2 / 1024) work-groups of 256 threads per problem, plus the relist
+// work-group of a compacted batch.
+void launch_merge(const TiledArgs &T, int k, hipStream_t st) {
+    hipLaunchKernelGGL(sk_tiled_merge_cols<kMergeColsThreads>, dim3(T.B + (T.order ? 1 : 0), T.MS),
+                       dim3(kMergeColsThreads), 0, st, T, k);
+}
 void launch_final(const TiledArgs &T, hipStream_t st) {
     if (T.d2 > 1024)
         hipLaunchKernelGGL(sk_tiled_final<1024>, dim3(T.B), dim3(1024), 0, st, T);
@@ -1649,7 +1710,7 @@ hipError_t run_wide(const TiledArgs &T, hipStream_t st) {
         for (int k = 1; k <= T.n_iter; ++k) {
             hipLaunchKernelGGL(sk_wide_rows<false>, rg, rblk, 0, st, T, k);
             hipLaunchKernelGGL(sk_wide_cols<false>, cg, blk, 0, st, T, k);
-            if (k < T.n_iter) hipLaunchKernelGGL(sk_tiled_merge_cols<1024>, dim3(T.B), dim3(1024), 0, st, T, k);
+            if (k < T.n_iter) launch_merge(T, k, st);
         }
     }
     hipLaunchKernelGGL(sk_wide_rows<true>, rg, rblk, 0, st, T, 0);
@@ -1670,13 +1731,7 @@ hipError_t run_sequence(const TiledArgs &T, hipStream_t st, Sweep sweep, Stats s
         hipLaunchKernelGGL(sk_tiled_merge_exact, dim3(T.JC, T.B), mblk, 0, st, T);
         for (int k = 1; k <= T.n_iter; ++k) {
             sweep(k);
-            if (k < T.n_iter) {
-                const dim3 mg(T.B + (T.order ? 1 : 0));
-                if (T.d2 > 1024)
-                    hipLaunchKernelGGL(sk_tiled_merge_cols<1024>, mg, dim3(1024), 0, st, T, k);
-                else
-                    hipLaunchKernelGGL(sk_tiled_merge_cols<256>, mg, dim3(256), 0, st, T, k);
-            }
+            if (k < T.n_iter) launch_merge(T, k, st);
         }
     }
     stats();
@@ -1837,6 +1892,19 @@ TiledArgs tiled_args(const FwdArgs &a, int kind, void *ws, Layout *Lout) {
     T.sync = T.state + a.B;
     T.order = nullptr;
     T.nlive = nullptr;
+    T.MS = merge_slices(a.d2);
+    T.stopacc = T.MS > 1 ? reinterpret_cast<unsigned long long *>(base + L.stopacc) : nullptr;
+    // Fixed point of the split merge's stop test: parts clamped to
+    // fx_cap = 2^p >= max(8, 2 tol) at 2^(48 - p - ceil(log2 MS)) units per
+    // unit of error, so that the sum of MS parts stays below 2^48 and never
+    // carries into the count.
+    int p = 3;
+    while (p < 60 && std::ldexp(1.0, p) < 2.0 * (double)a.tol) ++p;
+    int lms = 0;
+    while ((1 << lms) < T.MS) ++lms;
+    T.fx_cap = (float)std::ldexp(1.0, p);
+    T.fx_scale = std::ldexp(1.0, kFxCountShift - 1 - p - lms);
+    T.fx_tol = (double)a.tol * T.fx_scale;
     T.alpha_out = a.alpha;
     T.beta_out = a.beta;
     T.loss_out = a.loss;
@@ -1949,8 +2017,8 @@ int tiled_describe(const FwdArgs &a, char *buf, size_t len) {
     }
     char mrg[128];
     if (merge)
-        snprintf(mrg, sizeof mrg, "sk_tiled_merge_cols<%d> after each sweep (one work-group per problem)",
-                 kind == kKindWide || a.d2 > 1024 ? 1024 : 256);
+        snprintf(mrg, sizeof mrg, "sk_tiled_merge_cols<%d> after each sweep (%d work-group%s per problem)",
+                 kMergeColsThreads, merge_slices(a.d2), merge_slices(a.d2) == 1 ? "" : "s");
     else
         snprintf(mrg, sizeof mrg, "the merge folded into the next sweep");
     const bool compact = W && a.tol > 0.f && a.select != SK_SELECT_NO_COMPACTION;

@@ -619,6 +619,27 @@ def test_shared_sweep_early_stop_compaction():
         np.testing.assert_array_equal(gpu[k], plain[k])
 
 
+def test_split_merge_early_stop():
+    """Rows wider than 1024 columns: the merge after each sweep runs several
+    work-groups per problem, and the last of them to finish takes the stop
+    decision from their parts added in a fixed order.  Problems stop at
+    different iterations; parity with the oracle at the GPU's counts, the same
+    bits on a second run and without compaction."""
+    prob = workloads.random_problem(seed=611, B=12, d1=200, d2=2300, lam=0.05, n_iter=300, tol=1e-3,
+                                    zero_frac=0.1, cost="grid1d")
+    set_form("nocompact")
+    plain = _gpu(prob)
+    set_form("default")
+    gpu, ref = check_forward(prob)
+    again = _gpu(prob)
+    its = gpu["iters"]
+    _say(f"   iterations {sorted(its.tolist())}")
+    assert (its < prob.n_iter).sum() >= prob.B - 2 and len(set(its.tolist())) > 3, its
+    for k in plain:
+        np.testing.assert_array_equal(gpu[k], plain[k])
+        np.testing.assert_array_equal(gpu[k], again[k])
+
+
 # ---------------------------------------------------------------- randomized resident problems
 
 def test_random_resident_problems():
