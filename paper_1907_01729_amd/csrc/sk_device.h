@@ -22,6 +22,29 @@ constexpr float kSumHi = 1.84467440737095516e19f;   // 2^64
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
+// s_setprio with a level computed at run time or only after unrolling (0..3).
+__device__ __forceinline__ void set_issue_priority(int p) {
+    if (p <= 0)
+        __builtin_amdgcn_s_setprio(0);
+    else if (p == 1)
+        __builtin_amdgcn_s_setprio(1);
+    else if (p == 2)
+        __builtin_amdgcn_s_setprio(2);
+    else
+        __builtin_amdgcn_s_setprio(3);
+}
+
+// Issue-priority base of iteration k of n in a kernel that runs a whole
+// problem's iteration in one launch: 2 before the last eighth of the
+// iterations, 0 in it.  Two wavefronts of different problems share a SIMD and
+// have the same work; at equal priority the older one issues first, finishes
+// early and leaves the younger alone on the SIMD for the rest.  A wavefront
+// that reaches the last eighth first drops below the other until it gets
+// there too, so both end nearly together.  Phases of an iteration add 0 or 1.
+// (Measured on the log-domain kernel: 3 % on 1024 problems of 100 x 100; the
+// plain-form kernels, whose iterations are short, ran slower with it.)
+__device__ __forceinline__ int progress_priority(int k, int n) { return k < n - n / 8 ? 2 : 0; }
+
 // v_exp_f32 / v_log_f32: base-2 hardware transcendentals.
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float lg2(float x) { return __builtin_amdgcn_logf(x); }

@@ -183,12 +183,13 @@ __device__ __forceinline__ void resident_log_wave(const FwdArgs &A, float *pool)
         __syncthreads();
         for (int k = 1;; ++k) {
             float(&rd)[2][2] = red[k & 1];
+            const int pb = progress_priority(k, n_iter);
             // ---- u-update of iteration k: row sums of the plan e_ij
             float ar[H], bc[N], x[H];
             read_rows(rowa, ar);
             read_cols(bc);
             float e[KEEP ? H : 1][KEEP ? N : 1];
-            __builtin_amdgcn_s_setprio(0);
+            set_issue_priority(pb);
 #pragma unroll
             for (int ii = 0; ii < H; ++ii) {
                 if constexpr (KEEP) {
@@ -202,7 +203,7 @@ __device__ __forceinline__ void resident_log_wave(const FwdArgs &A, float *pool)
                     x[ii] = xs;
                 }
             }
-            __builtin_amdgcn_s_setprio(3);
+            set_issue_priority(pb + 1);
             const float R = row_totals<H>(x, tb, p, q);
             float f = 0.f, rerr = 0.f;
             bool bad = false;
@@ -286,7 +287,7 @@ __device__ __forceinline__ void resident_log_wave(const FwdArgs &A, float *pool)
                         fr[ii] = rb ? 1.f : fr[ii];
                     }
                 }
-                __builtin_amdgcn_s_setprio(0);
+                set_issue_priority(pb);
 #pragma unroll
                 for (int t = 0; t < N; ++t) {
                     float acc = e[0][t] * fr[0];
@@ -294,18 +295,18 @@ __device__ __forceinline__ void resident_log_wave(const FwdArgs &A, float *pool)
                     for (int ii = 1; ii < H; ++ii) acc = __builtin_fmaf(e[ii][t], fr[ii], acc);
                     y[t] = acc;
                 }
-                __builtin_amdgcn_s_setprio(3);
+                set_issue_priority(pb + 1);
             } else {
                 float an[H];
                 read_rows(rowa, an);
-                __builtin_amdgcn_s_setprio(0);
+                set_issue_priority(pb);
 #pragma unroll
                 for (int t = 0; t < N; ++t) y[t] = 0.f;
 #pragma unroll
                 for (int ii = 0; ii < H; ++ii)
 #pragma unroll
                     for (int t = 0; t < N; ++t) y[t] += ex2((an[ii] + bc[t]) + L[ii][t]);
-                __builtin_amdgcn_s_setprio(3);
+                set_issue_priority(pb + 1);
             }
 #pragma unroll
             for (int t = 0; t < N; ++t) cp[partial_at(w, p, q, t)] = y[t];

@@ -915,18 +915,6 @@ __device__ __forceinline__ float lane_get(float v, int src) {
     return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
 }
 
-// s_setprio with a level known only after unrolling (0..3).
-__device__ __forceinline__ void set_issue_priority(int p) {
-    if (p <= 0)
-        __builtin_amdgcn_s_setprio(0);
-    else if (p == 1)
-        __builtin_amdgcn_s_setprio(1);
-    else if (p == 2)
-        __builtin_amdgcn_s_setprio(2);
-    else
-        __builtin_amdgcn_s_setprio(3);
-}
-
 template <int NCW, int W, int RS, int RB, bool VEC4, bool STATS>
 __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int k) {
     constexpr int D2P = NCW * 64;  // LDS row length (columns beyond d2 hold kPadC)
@@ -1071,8 +1059,14 @@ __global__ __launch_bounds__(64 * W) void sk_tiled_sweep_shared(TiledArgs T, int
                 // (3 for the first rows, 0 for the last): of the wavefronts
                 // sharing a SIMD, the one behind issues first, so they reach
                 // the chunk's barrier together instead of the oldest one
-                // finishing early and leaving the SIMD to the other.
-                set_issue_priority(3 - rb * 4 / RS);
+                // finishing early and leaving the SIMD to the other.  With
+                // two batches per chunk the second bit is the block's
+                // progress: the last quarter of the chunks run two levels
+                // lower, so that of two work-groups sharing a CU the one
+                // ahead yields to the other near the end (3.8 % on the image
+                // batch, whose CUs hold two work-groups each).
+                set_issue_priority(RS / RB == 2 ? (rb == 0 ? 1 : 0) + (ch < nchunk - (nchunk + 3) / 4 ? 2 : 0)
+                                                : 3 - rb * 4 / RS);
 #pragma unroll
                 for (int g = 0; g < NG; ++g) {
                     if (g + 1 < NG) read_group(g + 1);
