@@ -10,10 +10,10 @@
 // (One exponential per cell per iteration; see the resident kernel for why the
 // current potential is a valid logsumexp shift.)  Column partials of a
 // work-group's wavefronts are combined in LDS; the row blocks' partials are
-// summed in a fixed order (no float atomics) by one work-group per problem
-// (sk_tiled_merge_cols), which also performs the v-update and takes the
-// marginal error.  The streaming sweep (per-sample cost) folds that merge into
-// the start of the next sweep instead.
+// summed in a fixed order (no float atomics) by one work-group per problem and
+// 1024 columns (sk_tiled_merge_cols), which also performs the v-update and
+// takes the marginal error.  The streaming sweep (per-sample cost) folds that
+// merge into the start of the next sweep instead.
 //
 // Launch sequence for n iterations:
 //   init                 a^0 = 0 on supp(mu), -inf off it; stop flags cleared
@@ -27,8 +27,7 @@
 // iteration k (column part summed there, by several work-groups above 1024
 // columns that combine their parts in one fixed-point atomic; row part from
 // the sweep's double-buffered row-block partials) and records K = k in the
-// stop flag,
-// which every later sweep and merge honours.  In the streaming sweep every
+// stop flag, which every later sweep and merge honours.  In the streaming sweep every
 // work-group of b sums the same partials in the same order, so all take the
 // same decision, and the first row block records it.
 #include <stdio.h>
