@@ -638,6 +638,13 @@ def test_split_merge_early_stop():
     for k in plain:
         np.testing.assert_array_equal(gpu[k], plain[k])
         np.testing.assert_array_equal(gpu[k], again[k])
+    # A tolerance above every possible first error (at most 2 for unit masses):
+    # parts are clamped at 2^p >= 2 tol, and every problem stops after one
+    # iteration, as in the oracle.
+    prob.tol = 5.0
+    one = _gpu(prob)
+    assert np.all(one["iters"] == 1), one["iters"]
+    check_forward(prob, gpu=one)
 
 
 # ---------------------------------------------------------------- randomized resident problems
@@ -770,7 +777,7 @@ def test_wide_grid_image_sampled():
     check_backward(prob, gpu, ref, idx=idx)
 
 
-@pytest.mark.parametrize("B,d1,d2", [(6, 40, 30), (5, 300, 260), (4, 150, 4100)])
+@pytest.mark.parametrize("B,d1,d2", [(6, 40, 30), (5, 300, 260), (5, 200, 2000), (4, 150, 4100)])
 def test_non_finite_cost_propagates(B, d1, d2):
     """A NaN in one problem's cost (per-sample costs): that problem's loss and
     error are not finite and it runs every iteration (its error is never
