@@ -69,6 +69,16 @@ def test_noalloc_early_stop_and_resident():
     _check(second)
 
 
+def test_noalloc_split_merge_twice():
+    """Rows wider than 1024 columns with an early stop, twice in a row on the
+    same scratch: the merge's per-problem stop accumulators left by the first
+    call are cleared before the second uses them."""
+    prob = workloads.random_problem(seed=904, B=6, d1=150, d2=2100, lam=0.05, n_iter=120, tol=1e-3,
+                                    cost="grid1d")
+    _check(prob)
+    _check(prob)
+
+
 def test_noalloc_rejects_problems_beyond_the_scratch():
     """The grid workload's workspace exceeds the fixed array: refused with
     SK_ERR_WORKSPACE before any launch (no allocation, no partial result)."""
